@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Benchmark: chunked-prefill causal attention on one MI355X.
+
+One step is one layer's attention over a whole synthetic prompt, chunk by chunk
+in order (chunk k: plan on the host, then the attention kernel and -- when the
+key range is split -- the merge pass), with every input resident in HBM. The
+value is the whole job's algorithmic rate: FLOPs of both GEMMs over the visible
+(query, key) pairs, 2*Hq*(dqk+dv)*(C*p + C*(C+1)/2) for a chunk of C queries at
+prefix p, divided by the wall time of the timed steps.
+
+Besides the contract line it reports, per chunk, the median latency against the
+prefix length (the cost curve of sections 4 and 5.1 of the paper) with a
+least-squares fit t_k = a + b*k, the residual of the balance identity of Eq. (3)
+(t_{k-1} + t_{k+1} - 2 t_k), a roofline entry for the attention kernel (timed
+with HIP events on the launch stream) and the fp64 oracle's rate on the host
+cores over a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload gqa|mla|long|mixed|tiny]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "chunked-prefill attention TFLOP/s (% bf16 MFMA peak) + per-chunk latency vs prefix"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+DEFAULT_STEPS = {"tiny": 50, "gqa": 50, "mla": 5, "long": 2, "mixed": 2}
+DEFAULT_WARMUP = {"tiny": 5, "gqa": 5, "mla": 1, "long": 1, "mixed": 1}
+
+
+def chunk_flops(w, cu, pre):
+    """Algorithmic FLOPs of one chunk: both GEMMs over visible pairs."""
+    pairs = 0
+    for s in range(len(pre)):
+        n = int(cu[s + 1] - cu[s])
+        p = int(pre[s])
+        pairs += n * p + n * (n + 1) // 2
+    return 2.0 * w.hq * (w.dqk + w.dv) * pairs, pairs
+
+
+def chunk_bytes(w, cu, pre):
+    """Algorithmic HBM bytes of one chunk: K/V read once, Q read, out and lse written."""
+    kv_rows = sum(int(pre[s]) + int(cu[s + 1] - cu[s]) for s in range(len(pre)))
+    tok = int(cu[-1])
+    return (kv_rows * w.hkv * (w.dqk + w.dv) * 2 + tok * w.hq * w.dqk * 2
+            + tok * w.hq * w.dv * 2 + tok * w.hq * 4)
+
+
+def fit_line(xs, ys):
+    n = len(xs)
+    if n < 2:
+        return None
+    mx, my = sum(xs) / n, sum(ys) / n
+    sxx = sum((x - mx) ** 2 for x in xs)
+    sxy = sum((x - mx) * (y - my) for x, y in zip(xs, ys))
+    b = sxy / sxx if sxx else 0.0
+    a = my - b * mx
+    ss_tot = sum((y - my) ** 2 for y in ys)
+    ss_res = sum((y - (a + b * x)) ** 2 for x, y in zip(xs, ys))
+    r2 = 1.0 - ss_res / ss_tot if ss_tot else 1.0
+    return {"a_ms": a, "b_ms": b, "b_over_a": (b / a) if a else None, "r2": r2}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(w, q, k, v, chunks, budget_s=12.0):
+    """Time the fp64 oracle on the host on a bounded sample of the last chunk's items."""
+    import numpy as np
+    import oracle
+    from paper_2608_26523_amd import workloads as W
+    oracle.build(force=False)
+    kidx = chunks - 1
+    t0, cu, kvs, pre = W.chunk_segments(w, kidx)
+    tok = int(cu[-1])
+    rng = np.random.default_rng(1234)
+    # one kv head's group of query heads keeps the host copy small
+    g = w.group
+    kvh = 0
+    hi = max(int(kvs[s] + pre[s] + cu[s + 1] - cu[s]) for s in range(len(pre)))
+    qh = q[t0:t0 + tok, kvh * g:(kvh + 1) * g].cpu()
+    kh = k[:hi, kvh:kvh + 1].cpu()
+    vh = v[:hi, kvh:kvh + 1].cpu()
+    threads = oracle.default_threads()
+    done_flops, done_items, elapsed = 0.0, 0, 0.0
+    batch = max(threads * 2, 16)
+    while elapsed < budget_s:
+        rows = rng.integers(0, tok, size=batch)
+        heads = rng.integers(0, g, size=batch).astype(np.int32)
+        seg = np.searchsorted(cu, rows, side="right") - 1
+        pos = np.asarray(pre)[seg] + rows - np.asarray(cu)[seg]
+        t = time.perf_counter()
+        oracle.attention(qh, kh, vh, cu, kvs, pre, rows=rows, heads=heads,
+                         scale=w.scale, n_threads=threads)
+        elapsed += time.perf_counter() - t
+        done_flops += float(np.sum(2.0 * (w.dqk + w.dv) * (pos + 1)))
+        done_items += batch
+    return {"value": done_flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "%d random (row, head) items of chunk %d (prefix %d) in %.1f s, "
+                      "fp64, %s" % (done_items, kidx, int(pre[0]), elapsed, cpu_model())}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=0)
+    ap.add_argument("--warmup", type=int, default=-1)
+    ap.add_argument("--workload", default="gqa")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--chunks", type=int, default=0, help="run only the first N chunks")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_26523_amd import workloads as W
+    from paper_2608_26523_amd.attention import ChunkAttention
+
+    w = W.get(args.workload)
+    steps = args.steps or DEFAULT_STEPS[w.name]
+    warmup = args.warmup if args.warmup >= 0 else DEFAULT_WARMUP[w.name]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    q, k, v = W.make_inputs(w, dev)
+    S = q.shape[0]
+    out = torch.empty((S, w.hq, w.dv), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((w.hq, S), dtype=torch.float32, device=dev)
+    nchunks = W.num_chunks(w)
+    if args.chunks:
+        nchunks = min(nchunks, args.chunks)
+    segs = [W.chunk_segments(w, c) for c in range(nchunks)]
+    attn = [ChunkAttention(w.hq, w.hkv, w.dqk, w.dv, max_chunk_tokens=w.chunk,
+                           max_kv_len=S, num_splits=w.num_splits) for _ in range(nchunks)]
+    flops = [chunk_flops(w, cu, pre)[0] for (_, cu, _, pre) in segs]
+    nbytes = [chunk_bytes(w, cu, pre) for (_, cu, _, pre) in segs]
+    stream = torch.cuda.current_stream(dev)
+
+    def step(events=None):
+        for c, (t0, cu, kvs, pre) in enumerate(segs):
+            a = attn[c]
+            a.plan(cu, kvs, pre)
+            tok = int(cu[-1])
+            if events is not None:
+                events[c][0].record(stream)
+            a.run(q[t0:t0 + tok], k, v, out[t0:t0 + tok], lse[:, t0:t0 + tok], stream=stream)
+            if events is not None:
+                events[c][1].record(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+           for _ in range(nchunks)] for _ in range(steps)]
+    t_start = time.perf_counter()
+    for s in range(steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+
+    per_chunk = [[ev[s][c][0].elapsed_time(ev[s][c][1]) for s in range(steps)]
+                 for c in range(nchunks)]
+    med = [statistics.median(x) for x in per_chunk]
+    mean = [statistics.fmean(x) for x in per_chunk]
+    total_flops = sum(flops)
+    ms_per_step = elapsed * 1e3 / steps
+    value = total_flops * steps / elapsed / 1e12
+    kernel_ms = statistics.fmean(mean)                    # average launch duration
+    achieved = (total_flops / nchunks) / (kernel_ms * 1e-3) / 1e12
+    splits = [attn[c].info().num_splits for c in range(nchunks)]
+
+    prefix = [int(pre[0]) if len(pre) == 1 else None for (_, _, _, pre) in segs]
+    fit = fit_line(list(range(nchunks)), med) if w.n_requests == 1 else None
+    eq3 = None
+    if w.n_requests == 1 and nchunks >= 3:
+        res = [(med[i - 1] + med[i + 1] - 2 * med[i]) / med[i] for i in range(1, nchunks - 1)]
+        eq3 = {"mean_rel_residual": statistics.fmean(res), "max_abs_rel_residual": max(abs(r) for r in res)}
+    res = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "tokens": S, "chunk": w.chunk, "chunks": nchunks,
+                   "requests": w.n_requests, "num_q_heads": w.hq, "num_kv_heads": w.hkv,
+                   "head_dim_qk": w.dqk, "head_dim_v": w.dv, "splits": max(splits),
+                   "parallelism": "none (1 GPU)"},
+        "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None,
+                     "kernel": "attn_fwd_kernel", "avg_launch_ms": round(kernel_ms, 4),
+                     "flops_per_launch": total_flops / nchunks,
+                     "algorithmic_bytes_per_launch": sum(nbytes) / nchunks},
+        "per_chunk": {"prefix_tokens": prefix, "median_ms": [round(x, 4) for x in med],
+                      "tflops": [round(f / (m * 1e-3) / 1e12, 2) for f, m in zip(flops, med)],
+                      "splits": splits, "fit": fit, "eq3_residual": eq3},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, q, k, v, nchunks)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

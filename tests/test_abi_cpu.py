@@ -1,0 +1,215 @@
+"""The C ABI on the host (no GPU): exports, planner invariants, argument checks."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_26523_amd import binding as B
+from paper_2608_26523_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vpp_chunk_attn.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(vpp_\w+)\s*\(", text)))
+
+
+def test_header_symbols_exported():
+    lib = B.load()
+    names = header_functions()
+    assert "vpp_chunk_attn_plan" in names and "vpp_chunk_attn_run" in names
+    for n in names:
+        assert hasattr(lib, n), "symbol %s declared in the header is not exported" % n
+    assert sorted(B.EXPORTED) == names
+
+
+def cfg(hq=8, hkv=2, dqk=128, dv=128, max_tok=4096, max_seg=16, max_kv=1 << 20, splits=-1,
+        causal=1, scale=0.0):
+    return B.Config(num_q_heads=hq, num_kv_heads=hkv, head_dim_qk=dqk, head_dim_v=dv,
+                    softmax_scale=scale, causal=causal, max_chunk_tokens=max_tok,
+                    max_segments=max_seg, max_kv_len=max_kv, num_splits=splits)
+
+
+def plan_status(c, cu, ks, pl):
+    lib = B.load()
+    cu = np.ascontiguousarray(cu, dtype=np.int32)
+    ks = np.ascontiguousarray(ks, dtype=np.int64)
+    pl = np.ascontiguousarray(pl, dtype=np.int64)
+    h = ctypes.c_void_p(None)
+    ws = ctypes.c_size_t(0)
+    st = lib.vpp_chunk_attn_plan(ctypes.byref(c) if c is not None else None, len(ks),
+                                 cu.ctypes.data, ks.ctypes.data, pl.ctypes.data,
+                                 ctypes.byref(h), ctypes.byref(ws))
+    if h.value:
+        B.vpp_chunk_attn_destroy(h.value)
+    return st
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(hq=6, hkv=4), B.VPP_ERR_INVALID_ARG),
+    (dict(dqk=96, dv=96), B.VPP_ERR_UNSUPPORTED),
+    (dict(dqk=128, dv=64), B.VPP_ERR_UNSUPPORTED),
+    (dict(causal=0), B.VPP_ERR_UNSUPPORTED),
+    (dict(splits=0), B.VPP_ERR_INVALID_ARG),
+    (dict(splits=17), B.VPP_ERR_INVALID_ARG),
+    (dict(scale=-1.0), B.VPP_ERR_INVALID_ARG),
+    (dict(max_tok=0), B.VPP_ERR_INVALID_ARG),
+])
+def test_config_errors(bad, status):
+    assert plan_status(cfg(**bad), [0, 10], [0], [0]) == status
+
+
+@pytest.mark.parametrize("cu,ks,pl", [
+    ([1, 10], [0], [0]),                 # cu_q[0] != 0
+    ([0, 10, 5], [0, 20], [0, 0]),       # decreasing
+    ([0, 10], [-1], [0]),                # negative kv_start
+    ([0, 10], [0], [-5]),                # negative prefix
+    ([0, 5000], [0], [0]),               # more rows than max_chunk_tokens
+    ([0, 10], [(1 << 20) - 5], [0]),     # runs past max_kv_len
+])
+def test_metadata_errors(cu, ks, pl):
+    assert plan_status(cfg(), cu, ks, pl) == B.VPP_ERR_INVALID_ARG
+
+
+def test_too_many_segments_and_null_args():
+    assert plan_status(cfg(max_seg=2), [0, 1, 2, 3], [0, 1, 2], [0, 0, 0]) == B.VPP_ERR_INVALID_ARG
+    lib = B.load()
+    ws = ctypes.c_size_t(0)
+    h = ctypes.c_void_p(None)
+    assert lib.vpp_chunk_attn_plan(None, 1, None, None, None, ctypes.byref(h),
+                                   ctypes.byref(ws)) == B.VPP_ERR_INVALID_ARG
+    assert lib.vpp_chunk_attn_plan_info(None, None) == B.VPP_ERR_INVALID_ARG
+    assert B.vpp_status_str(B.VPP_ERR_WORKSPACE) == "workspace too small"
+    lib.vpp_chunk_attn_destroy(None)
+
+
+def test_refill_must_keep_config():
+    h, _ = B.vpp_chunk_attn_plan(cfg(), [0, 100], [0], [0])
+    try:
+        B.vpp_chunk_attn_plan(None, [0, 300], [0], [500], plan=h)      # refill, same config
+        assert B.vpp_chunk_attn_plan_info(h).num_tokens == 300
+        with pytest.raises(B.VppError):
+            B.vpp_chunk_attn_plan(cfg(hq=16), [0, 10], [0], [0], plan=h)
+    finally:
+        B.vpp_chunk_attn_destroy(h)
+
+
+def check_plan(c, cu, ks, pl):
+    h, ws = B.vpp_chunk_attn_plan(c, cu, ks, pl)
+    try:
+        info = B.vpp_chunk_attn_plan_info(h)
+        items = B.vpp_chunk_attn_plan_items(h)
+    finally:
+        B.vpp_chunk_attn_destroy(h)
+    bm, bn, n = info.block_m, info.block_n, info.num_splits
+    assert info.num_work_items == len(items) == info.num_tiles * n
+    assert ws == info.workspace_bytes and ws >= len(items) * 32
+    # longest key range first
+    lens = items["key_end"] - items["key_begin"]
+    assert np.all(np.diff(lens) <= 0)
+    # tiles: rows partition the chunk, positions and bases follow the segments
+    tiles = {}
+    for it in items:
+        tiles.setdefault(int(it["row0"]), []).append(it)
+    covered = np.zeros(int(cu[-1]), dtype=np.int32)
+    pairs = 0
+    for row0, its in tiles.items():
+        assert len(its) == n
+        t = its[0]
+        assert 1 <= t["nrows"] <= bm
+        covered[row0:row0 + t["nrows"]] += 1
+        s = int(np.searchsorted(cu, row0, side="right") - 1)
+        assert row0 + t["nrows"] <= cu[s + 1], "a tile crosses a segment boundary"
+        assert t["pos0"] == pl[s] + row0 - cu[s]
+        assert t["kv_base"] == ks[s]
+        # splits cover [0, last position + 1) exactly, in order, tile-aligned inside
+        rng = sorted((int(x["split"]), int(x["key_begin"]), int(x["key_end"])) for x in its)
+        assert [r[0] for r in rng] == list(range(n))
+        assert rng[0][1] == 0 and rng[-1][2] == t["pos0"] + t["nrows"]
+        for a, b in zip(rng, rng[1:]):
+            assert a[2] == b[1] and a[2] % bn == 0
+        pairs += int(t["nrows"]) * int(t["pos0"]) + int(t["nrows"]) * (int(t["nrows"]) + 1) // 2
+    assert np.all(covered == 1)
+    assert info.pairs == pairs
+    return info
+
+
+@pytest.mark.parametrize("name", ["tiny", "gqa", "mla", "long"])
+def test_plan_workload_chunks(name):
+    w = W.get(name)
+    c = cfg(hq=w.hq, hkv=w.hkv, dqk=w.dqk, dv=w.dv, max_tok=w.chunk, max_kv=w.seq_len,
+            splits=w.num_splits)
+    for k in sorted({0, 1, W.num_chunks(w) - 1}):
+        _, cu, ks, pl = W.chunk_segments(w, k)
+        info = check_plan(c, cu, ks, pl)
+        if w.num_splits > 0:
+            assert info.num_splits == w.num_splits
+
+
+def test_plan_mixed_chunks():
+    w = W.get("mixed")
+    c = cfg(hq=w.hq, hkv=w.hkv, dqk=w.dqk, dv=w.dv, max_tok=w.chunk,
+            max_kv=W.total_tokens(w), max_seg=256)
+    n = W.num_chunks(w)
+    multi = 0
+    for k in list(range(0, n, 23)) + [n - 1]:
+        _, cu, ks, pl = W.chunk_segments(w, k)
+        multi += len(ks) > 1
+        check_plan(c, cu, ks, pl)
+    assert multi > 0, "no sampled chunk spans a request boundary"
+
+
+@pytest.mark.parametrize("splits", [2, 3, 5, 16])
+def test_plan_forced_splits_ragged(splits):
+    c = cfg(splits=splits)
+    check_plan(c, [0, 1, 1, 130, 400], [0, 7, 7, 500], [63, 0, 1000, 37])
+
+
+def test_auto_split_only_when_few_workgroups():
+    # one tile x 8 heads with a long prefix: too few workgroups -> split
+    info = check_plan(cfg(), [0, 100], [0], [200000])
+    assert info.num_splits > 1
+    # a full 4096-row chunk over 32 heads: plenty of workgroups -> no split
+    info = check_plan(cfg(hq=32, hkv=8), [0, 4096], [0], [200000])
+    assert info.num_splits == 1
+
+
+def test_run_argument_checks_before_any_device_work():
+    """Errors the host can detect are returned before any HIP call (works without a GPU)."""
+    lib = B.load()
+    h, ws = B.vpp_chunk_attn_plan(cfg(), [0, 64], [0], [0])
+    try:
+        good = 1 << 20            # aligned fake addresses: never dereferenced on these paths
+        base = dict(q=good, qs=(8 * 128, 128), k=good, ks=(2 * 128, 128), v=good,
+                    vs=(2 * 128, 128), o=good, os=(8 * 128, 128), lse=0, lsh=0,
+                    ws=good, wsb=ws)
+
+        def call(**over):
+            a = dict(base)
+            a.update(over)
+            return lib.vpp_chunk_attn_run(h, a["q"], a["qs"][0], a["qs"][1], a["k"], a["ks"][0],
+                                          a["ks"][1], a["v"], a["vs"][0], a["vs"][1], a["o"],
+                                          a["os"][0], a["os"][1], a["lse"], a["lsh"], a["ws"],
+                                          a["wsb"], None)
+        assert call(q=0) == B.VPP_ERR_INVALID_ARG
+        assert call(k=good + 2) == B.VPP_ERR_INVALID_ARG
+        assert call(qs=(8 * 128 + 4, 128)) == B.VPP_ERR_INVALID_ARG
+        assert call(os=(0, 128)) == B.VPP_ERR_INVALID_ARG
+        assert call(lse=good, lsh=10) == B.VPP_ERR_INVALID_ARG        # stride < tokens
+        assert call(ws=0) == B.VPP_ERR_WORKSPACE
+        assert call(ws=good + 64) == B.VPP_ERR_WORKSPACE
+        assert call(wsb=ws - 1) == B.VPP_ERR_WORKSPACE
+        assert lib.vpp_chunk_attn_run(None, good, 1024, 128, good, 256, 128, good, 256, 128,
+                                      good, 1024, 128, 0, 0, good, ws, None) == B.VPP_ERR_INVALID_ARG
+    finally:
+        B.vpp_chunk_attn_destroy(h)
+
+
+def test_empty_chunk_plans_to_nothing():
+    info = check_plan(cfg(), [0, 0, 0], [0, 5], [3, 0])
+    assert info.num_work_items == 0 and info.num_tokens == 0
