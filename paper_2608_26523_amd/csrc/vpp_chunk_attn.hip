@@ -27,6 +27,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <type_traits>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -35,17 +36,27 @@
 
 namespace {
 
-constexpr int BM = 128;        // query rows per workgroup tile
+constexpr int BM = 256;        // query rows per workgroup tile (4 waves x 64 rows)
 constexpr int BN = 64;         // keys per inner step
-constexpr int NTHREADS = 256;  // 4 waves of 64
+constexpr int NWAVES = 4;
+constexpr int NTHREADS = 64 * NWAVES;
 constexpr int MAX_SPLITS = 16;
 constexpr int STAGING_SLOTS = 4;
+// Lazy rescale: the running max used for exp2 is refreshed only when a row's
+// max grows past it by more than this many powers of two; O and l share the
+// stale max, so the final quotient is unchanged and P stays <= 2^TAU.
+constexpr float LAZY_TAU = 8.0f;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16;
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
 
 typedef vpp_chunk_attn_work_item_t WorkItem;
 static_assert(sizeof(WorkItem) == 32, "work item layout");
@@ -68,23 +79,34 @@ struct AttnArgs {
     int32_t xcd_remap;
 };
 
-template <int DQK, int DV>
-struct Smem {
-    static constexpr int K_STRIDE = DQK + 8;  // 16-byte pad: conflict-free 16 B row reads
-    static constexpr int VT_STRIDE = BN + 4;  // 8-byte pad: conflict-free 8 B column reads
-    u16 k[BN * K_STRIDE];
-    u16 vt[DV * VT_STRIDE];
-};
+// LDS tiles: K [BN][DQK] and V [BN][DV] bf16, row-major in 16-byte granules,
+// granule index XOR-swizzled with (row & 7): the 8 rows a ds_read_b128 (K) or
+// ds_read_b64_tr_b16 (V) touches in one cycle then fall in 8 different bank
+// groups.
+__device__ __forceinline__ int swz(int row, int granule) { return granule ^ (row & 7); }
 
-__device__ __forceinline__ float wave_swap32_max(float x) {
-    return fmaxf(x, __shfl_xor(x, 32, 64));
+__device__ __forceinline__ float lane_swap32_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
-__device__ __forceinline__ float wave_swap32_add(float x) {
-    return x + __shfl_xor(x, 32, 64);
+__device__ __forceinline__ float lane_swap32_add(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__device__ __forceinline__ uint32_t half16(const u32x4& r, int c) {
-    return (r[c >> 1] >> ((c & 1) * 16)) & 0xFFFFu;
+// LDS-only workgroup barrier: orders LDS traffic without waiting for the
+// asynchronous global->LDS copies of the next stage.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// s_waitcnt with only vmcnt constrained (expcnt / lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
 // Launch-order index -> (item, head). With remapping on, the hardware's
@@ -102,13 +124,228 @@ __device__ __forceinline__ void work_coords(const AttnArgs& a, int& item, int& h
     item = (int)(L % a.num_items);
 }
 
+template <int DQK, int DV>
+struct Tiles {
+    static constexpr int KS = DQK / 16;          // MFMA k-steps of S^T = K Q^T
+    static constexpr int DB = DV / 32;           // 32-row blocks of O^T
+    static constexpr int KGR = DQK / 8;          // 16-byte granules per K row
+    static constexpr int VGR = DV / 8;
+    static constexpr int K_BYTES = BN * KGR * 16;
+    static constexpr int V_BYTES = BN * VGR * 16;
+    static constexpr int BYTES = 2 * K_BYTES + 2 * V_BYTES;  // double-buffered K and V
+    static constexpr int K_LOADS = BN * KGR / 64 / NWAVES;   // 16-byte loads per lane per tile
+    static constexpr int V_LOADS = BN * VGR / 64 / NWAVES;
+    static constexpr int NQK = 4 * KS;           // MFMAs of one S^T tile (2 key blocks x 2 query blocks)
+    static constexpr int NPV = 8 * DB;           // MFMAs of one O^T update (4 key groups x 2 query blocks)
+    static_assert(KGR % 8 == 0 && VGR % 8 == 0, "swizzle needs 8 granules per row");
+    static_assert(BN * KGR % (64 * NWAVES) == 0 && BN * VGR % (64 * NWAVES) == 0, "whole wave loads");
+};
+
+// S^T MFMA i of a tile: key block mb = 1 first, so that the block-0
+// accumulators of the next tile are written only after the softmax has
+// consumed this tile's block 0 and their registers can be reused.
+template <int KS>
+struct QkCoords {
+    static constexpr int mb(int i) { return 1 - i / (2 * KS); }
+    static constexpr int ks(int i) { return (i % (2 * KS)) >> 1; }
+    static constexpr int nb(int i) { return i & 1; }
+};
+
+// ---------------------------------------------------------------------------
+// Static instruction schedule of one key tile.
+//
+// One wave (one SIMD) runs, per tile, NQK MFMAs of the next tile's S^T, NPV
+// MFMAs of this tile's O^T update and the softmax of this tile in fp32 VALU
+// code. A wave issues in order, and VALU work issued between two MFMAs runs
+// while the matrix core is busy, so the softmax is cut into pieces spread
+// evenly over the MFMA slots:
+//   piece 0, 1          row max of query block 0 / 1 (and the lazy rescale decision)
+//   piece 2 + 2u + h    exp, row sum and bf16 packing of 4 elements of unit u, half h
+// where unit u = (key block mb, 16-key group hh, query block nb) = (u>>2, (u>>1)&1, u&1)
+// holds the 8 P values one O^T MFMA group consumes. O^T MFMAs of unit u are
+// placed only after its two pieces; all pieces finish before the last unit's
+// MFMAs, which therefore run alone at the end of the tile.
+// ---------------------------------------------------------------------------
+constexpr int N_PIECES = 18;
+constexpr int piece_weight(int k) { return k < 2 ? 140 : 92; }  // VALU cycles, measured rates
+
+template <int NQK, int NPV, int DB>
+struct Schedule {
+    // the last tile has no next S^T to overlap with: it opens with one
+    // VALU-only slot, then hides each unit's softmax under the previous unit's MFMAs
+    static constexpr int NS = NQK + NPV + (NQK == 0 ? 1 : 0);
+    int kind[NS] = {};       // 0: S^T MFMA, 1: O^T MFMA, 2: no MFMA
+    int index[NS] = {};      // S^T: see qk_coords; O^T: unit*DB + d
+    int pieces_end[NS] = {}; // VALU pieces issued after this slot: [pieces_end[s-1], pieces_end[s])
+    int rescale_before = 0;  // slot before which the (rare) O rescale check runs
+    constexpr Schedule() {
+        int done_at[N_PIECES] = {};
+        if constexpr (NQK == 0) {
+            kind[0] = 2;
+            for (int k = 0; k < 4; ++k) done_at[k] = 0;
+            for (int p = 0; p < NPV; ++p) {
+                kind[1 + p] = 1;
+                index[1 + p] = p;
+            }
+            for (int u = 1; u < 8; ++u) {  // unit u under unit u-1's MFMAs
+                const int first = 1 + (u - 1) * DB;
+                done_at[2 + 2 * u] = first;
+                done_at[3 + 2 * u] = first + (DB > 1 ? 1 : 0);
+            }
+        } else {
+            // slot by which each piece must be done: spread by weight over the
+            // slots before the last unit's MFMAs
+            int total = 0;
+            for (int k = 0; k < N_PIECES; ++k) total += piece_weight(k);
+            const int span = NS - DB;
+            int acc = 0;
+            for (int k = 0; k < N_PIECES; ++k) {
+                acc += piece_weight(k);
+                int s = (acc * span + total - 1) / total - 1;
+                done_at[k] = s < 0 ? 0 : s;
+            }
+            // MFMA order: an O^T MFMA as soon as its unit's pieces are done, else an S^T MFMA
+            int q = 0, p = 0;
+            for (int s = 0; s < NS; ++s) {
+                const int unit = p / DB;
+                const bool pv_ready = p < NPV && done_at[1] < s && done_at[2 + 2 * unit + 1] < s;
+                if (pv_ready || q >= NQK) {
+                    kind[s] = 1;
+                    index[s] = p++;
+                } else {
+                    kind[s] = 0;
+                    index[s] = q++;
+                }
+            }
+        }
+        for (int s = 0; s < NS; ++s) {
+            int n = 0;
+            for (int k = 0; k < N_PIECES; ++k) n += done_at[k] <= s;
+            pieces_end[s] = n;
+        }
+        rescale_before = NS;
+        for (int s = NS - 1; s >= 0; --s)
+            if (kind[s] == 1) rescale_before = s;
+    }
+    // every O^T MFMA comes after the pieces it depends on
+    constexpr bool valid() const {
+        for (int s = 0; s < NS; ++s) {
+            if (kind[s] != 1) continue;
+            const int unit = index[s] / DB;
+            const int before = s == 0 ? 0 : pieces_end[s - 1];
+            if (before < 2 + 2 * unit + 2) return false;
+        }
+        return pieces_end[NS - 1] == N_PIECES;
+    }
+};
+
+// The MFMAs are written as inline asm so that each operand stays in the
+// register file it belongs to for the whole loop: Q and the O accumulators in
+// AGPRs (only MFMAs touch them), S and P in VGPRs (the softmax reads and
+// writes them). The compiler cannot see the latency of these instructions, so
+// the schedule keeps the required distances itself: an S^T tile is read by
+// VALU code only in the next tile's step (after a barrier), O only after an
+// explicit drain, and the "s_nop 2" in front of an O^T MFMA covers a P operand
+// packed by VALU code just before it.
+#define MFMA_32x32x16_INIT(acc, a, b) \
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b))
+#define MFMA_32x32x16_ACC(acc, a, b) \
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b))
+#define MFMA_32x32x16_PV(acc, a, b) \
+    asm volatile("s_nop 2\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b))
+
+__device__ __forceinline__ void mfma_drain() {
+    // longer than the longest MFMA result latency: 3 x 16 wait states
+    asm volatile("s_nop 15\n\ts_nop 15\n\ts_nop 15" ::: "memory");
+}
+
+// Load the KS B-operand fragments of one query row (16 bytes each, 32 bytes
+// apart) straight into AGPRs, where only MFMAs read them. Loading through
+// VGPRs would leave a VGPR copy of Q alive across the whole loop.
+template <int KS>
+__device__ __forceinline__ void load_q_agpr(bf16x8 (&qf)[KS], const void* p) {
+    static_assert(KS == 4 || KS == 8 || KS == 12, "head dims 64, 128, 192");
+    if constexpr (KS == 4) {
+        asm volatile(
+            "global_load_dwordx4 %0, %4, off\n\t"
+            "global_load_dwordx4 %1, %4, off offset:32\n\t"
+            "global_load_dwordx4 %2, %4, off offset:64\n\t"
+            "global_load_dwordx4 %3, %4, off offset:96"
+            : "=a"(qf[0]), "=a"(qf[1]), "=a"(qf[2]), "=a"(qf[3])
+            : "v"(p) : "memory");
+    } else if constexpr (KS == 8) {
+        asm volatile(
+            "global_load_dwordx4 %0, %8, off\n\t"
+            "global_load_dwordx4 %1, %8, off offset:32\n\t"
+            "global_load_dwordx4 %2, %8, off offset:64\n\t"
+            "global_load_dwordx4 %3, %8, off offset:96\n\t"
+            "global_load_dwordx4 %4, %8, off offset:128\n\t"
+            "global_load_dwordx4 %5, %8, off offset:160\n\t"
+            "global_load_dwordx4 %6, %8, off offset:192\n\t"
+            "global_load_dwordx4 %7, %8, off offset:224"
+            : "=a"(qf[0]), "=a"(qf[1]), "=a"(qf[2]), "=a"(qf[3]), "=a"(qf[4]), "=a"(qf[5]),
+              "=a"(qf[6]), "=a"(qf[7])
+            : "v"(p) : "memory");
+    } else {
+        asm volatile(
+            "global_load_dwordx4 %0, %12, off\n\t"
+            "global_load_dwordx4 %1, %12, off offset:32\n\t"
+            "global_load_dwordx4 %2, %12, off offset:64\n\t"
+            "global_load_dwordx4 %3, %12, off offset:96\n\t"
+            "global_load_dwordx4 %4, %12, off offset:128\n\t"
+            "global_load_dwordx4 %5, %12, off offset:160\n\t"
+            "global_load_dwordx4 %6, %12, off offset:192\n\t"
+            "global_load_dwordx4 %7, %12, off offset:224\n\t"
+            "global_load_dwordx4 %8, %12, off offset:256\n\t"
+            "global_load_dwordx4 %9, %12, off offset:288\n\t"
+            "global_load_dwordx4 %10, %12, off offset:320\n\t"
+            "global_load_dwordx4 %11, %12, off offset:352"
+            : "=a"(qf[0]), "=a"(qf[1]), "=a"(qf[2]), "=a"(qf[3]), "=a"(qf[4]), "=a"(qf[5]),
+              "=a"(qf[6]), "=a"(qf[7]), "=a"(qf[8]), "=a"(qf[9]), "=a"(qf[10]), "=a"(qf[11])
+            : "v"(p) : "memory");
+    }
+}
+
+// o *= alpha for one 16-AGPR accumulator tile, in place, through a single
+// temporary VGPR (the accumulators never get a VGPR home).
+__device__ __forceinline__ void scale_agpr_tile(f32x16& o, float alpha) {
+    float e0 = o[0], e1 = o[1], e2 = o[2], e3 = o[3], e4 = o[4], e5 = o[5], e6 = o[6], e7 = o[7];
+    float e8 = o[8], e9 = o[9], e10 = o[10], e11 = o[11], e12 = o[12], e13 = o[13], e14 = o[14], e15 = o[15];
+    float tmp;
+#define SCALE_ONE(n) "v_accvgpr_read_b32 %16, %" #n "\n\ts_nop 1\n\tv_mul_f32 %16, %16, %17\n\ts_nop 1\n\tv_accvgpr_write_b32 %" #n ", %16\n\t"
+    asm volatile(SCALE_ONE(0) SCALE_ONE(1) SCALE_ONE(2) SCALE_ONE(3) SCALE_ONE(4) SCALE_ONE(5) SCALE_ONE(6)
+                 SCALE_ONE(7) SCALE_ONE(8) SCALE_ONE(9) SCALE_ONE(10) SCALE_ONE(11) SCALE_ONE(12) SCALE_ONE(13)
+                 SCALE_ONE(14) SCALE_ONE(15) "s_nop 1"
+                 : "+a"(e0), "+a"(e1), "+a"(e2), "+a"(e3), "+a"(e4), "+a"(e5), "+a"(e6), "+a"(e7), "+a"(e8),
+                   "+a"(e9), "+a"(e10), "+a"(e11), "+a"(e12), "+a"(e13), "+a"(e14), "+a"(e15), "=&v"(tmp)
+                 : "v"(alpha));
+#undef SCALE_ONE
+    o[0] = e0; o[1] = e1; o[2] = e2; o[3] = e3; o[4] = e4; o[5] = e5; o[6] = e6; o[7] = e7;
+    o[8] = e8; o[9] = e9; o[10] = e10; o[11] = e11; o[12] = e12; o[13] = e13; o[14] = e14; o[15] = e15;
+}
+
+template <int N, typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>()), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl<N>(f, std::make_integer_sequence<int, N>());
+}
+
 template <int DQK, int DV, bool SPLIT>
-__global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(AttnArgs a) {
-    __shared__ Smem<DQK, DV> sm;
-    constexpr int KS = DQK / 16;   // MFMA k-steps for S
-    constexpr int DB = DV / 32;    // 32-wide value blocks
-    constexpr int K_STRIDE = Smem<DQK, DV>::K_STRIDE;
-    constexpr int VT_STRIDE = Smem<DQK, DV>::VT_STRIDE;
+__global__ __attribute__((amdgpu_flat_work_group_size(NTHREADS, NTHREADS), amdgpu_waves_per_eu(1, 1)))
+void attn_fwd_kernel(AttnArgs a) {
+    typedef Tiles<DQK, DV> T;
+    constexpr int KS = T::KS;
+    constexpr int DB = T::DB;
+    typedef Schedule<T::NQK, T::NPV, DB> SchedFull;
+    typedef Schedule<0, T::NPV, DB> SchedLast;
+    static_assert(SchedFull().valid() && SchedLast().valid(), "tile schedule breaks a dependency");
+
+    __shared__ __attribute__((aligned(1024))) char smem[T::BYTES];
+    char* const kbuf0 = smem;
+    char* const vbuf0 = smem + 2 * T::K_BYTES;
 
     int item_id, h;
     work_coords(a, item_id, h);
@@ -120,167 +357,319 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(AttnArgs a) {
     const int lr = lane & 31;
     const int lg = lane >> 5;
 
-    // This lane's query row: B-operand fragments of Q in registers.
-    const int rloc = wave * 32 + lr;
-    const bool row_valid = rloc < it.nrows;
-    const int qpos = it.pos0 + rloc;
-    bf16x8 qf[KS];
-    {
-        const u16* qp = a.q + (int64_t)(it.row0 + (row_valid ? rloc : 0)) * a.q_st + (int64_t)h * a.q_sh;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            u32x4 raw = {0u, 0u, 0u, 0u};
-            if (row_valid) raw = *(const u32x4*)(qp + ks * 16 + lg * 8);
-            qf[ks] = __builtin_bit_cast(bf16x8, raw);
-        }
-    }
-    // last valid query position held by this wave (waves past nrows: none)
-    const int wave_rows = min(32, it.nrows - wave * 32);
-    const int wave_pos_last = it.pos0 + wave * 32 + wave_rows - 1;
-    const int wave_pos_first = it.pos0 + wave * 32;
-
-    float m_run = -INFINITY;  // running max of scaled scores (log2 units)
-    float l_run = 0.f;        // this lane's share of the softmax denominator
-    f32x16 o[DB];
-#pragma unroll
-    for (int d = 0; d < DB; ++d)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) o[d][i] = 0.f;
-
     const int kb = it.key_begin, ke = it.key_end;
     const u16* kbase = a.k + it.kv_base * a.k_st + (int64_t)hk * a.k_sh;
     const u16* vbase = a.v + it.kv_base * a.v_st + (int64_t)hk * a.v_sh;
+    const int ntiles = (ke - kb + BN - 1) / BN;
 
-    for (int kt = kb; kt < ke; kt += BN) {
-        __syncthreads();  // everyone is done reading the previous tile
-        // K tile: rows kt..kt+63 -> LDS row-major (zero past the key range)
-        for (int e = tid; e < BN * (DQK / 8); e += NTHREADS) {
-            const int r = e / (DQK / 8), c = e % (DQK / 8);
-            u32x4 val = {0u, 0u, 0u, 0u};
-            if (kt + r < ke) val = *(const u32x4*)(kbase + (int64_t)(kt + r) * a.k_st + c * 8);
-            *(u32x4*)(&sm.k[r * K_STRIDE + c * 8]) = val;
-        }
-        // V tile -> LDS transposed: each thread moves 4 keys x 8 value columns
-        for (int e = tid; e < (BN / 4) * (DV / 8); e += NTHREADS) {
-            const int dg = e % (DV / 8), kg = e / (DV / 8);
-            u32x4 r[4];
+    // This lane's two query rows (one per 32-column block of S^T), as B
+    // operands in AGPRs. Rows past the tile re-read its last row (their results
+    // are never stored), so every load stays inside q.
+    bf16x8 qf[2][KS];
+    int qlim[2];   // last key position the row may see, minus lg*4 (see masking)
+    bool qvalid[2];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int key = kt + kg * 4 + j;
-                r[j] = u32x4{0u, 0u, 0u, 0u};
-                if (key < ke) r[j] = *(const u32x4*)(vbase + (int64_t)key * a.v_st + dg * 8);
-            }
-#pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                u32x2 w;
-                w[0] = half16(r[0], c) | (half16(r[1], c) << 16);
-                w[1] = half16(r[2], c) | (half16(r[3], c) << 16);
-                *(u32x2*)(&sm.vt[(dg * 8 + c) * VT_STRIDE + kg * 4]) = w;
-            }
-        }
-        __syncthreads();
+    for (int nb = 0; nb < 2; ++nb) {
+        const int rloc = wave * 64 + nb * 32 + lr;
+        qvalid[nb] = rloc < it.nrows;
+        qlim[nb] = min(it.pos0 + rloc, ke - 1) - lg * 4;
+        const u16* qp = a.q + (int64_t)(it.row0 + min(rloc, it.nrows - 1)) * a.q_st + (int64_t)h * a.q_sh + lg * 8;
+        load_q_agpr<KS>(qf[nb], qp);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
-        if (kt > wave_pos_last) continue;  // every key of this tile is after this wave's queries
-
-        // S^T = K Q^T for 64 keys x 32 queries
-        f32x16 s[2];
+    // Global->LDS copy of one tile: per-lane element offsets are fixed and the
+    // tile base kt*stride is wave-uniform. In the last tile, rows past the key
+    // range are not loaded: their LDS rows keep older, finite data (the V
+    // buffers are zeroed first), and they are masked to probability 0.
+    uint32_t k_src[T::K_LOADS], v_src[T::V_LOADS];  // byte offsets from the tile base
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
+    for (int t = 0; t < T::K_LOADS; ++t) {
+        const int slot = t * NTHREADS + tid;
+        const int row = slot / T::KGR, gs = slot % T::KGR;
+        k_src[t] = (uint32_t)(row * (int)a.k_st + swz(row, gs) * 8) * 2u;
+    }
 #pragma unroll
-            for (int i = 0; i < 16; ++i) s[mb][i] = 0.f;
-            const u16* krow = &sm.k[(mb * 32 + lr) * K_STRIDE + lg * 8];
+    for (int t = 0; t < T::V_LOADS; ++t) {
+        const int slot = t * NTHREADS + tid;
+        const int row = slot / T::VGR, gs = slot % T::VGR;
+        v_src[t] = (uint32_t)(row * (int)a.v_st + swz(row, gs) * 8) * 2u;
+    }
+    // Slot t*NTHREADS + tid of a tile holds row slot / GR: in the last tile it is
+    // loaded only when that row is inside the key range, i.e. when the slot index
+    // is below (ke - kt) * GR.
+    auto issue_k = [&](char* buf, int kt) {
+        const char* b = (const char*)(kbase + (int64_t)kt * a.k_st);
+        const int lim = kt + BN <= ke ? NTHREADS * T::K_LOADS : (ke - kt) * T::KGR;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 af = __builtin_bit_cast(bf16x8, *(const u32x4*)(krow + ks * 16));
-                s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[ks], s[mb], 0, 0, 0);
-            }
-        }
-
-        // scale, mask, running max
-        const bool need_mask = (kt + BN - 1 > wave_pos_first) || (kt + BN > ke);
-        float mloc = -INFINITY;
+        for (int t = 0; t < T::K_LOADS; ++t)
+            if (t * NTHREADS + tid < lim)
+                __builtin_amdgcn_global_load_lds((glb_void_t*)(b + k_src[t]),
+                                                 (lds_void_t*)(buf + (t * NWAVES + wave) * 1024), 16, 0, 0);
+    };
+    auto issue_v = [&](char* buf, int kt) {
+        const char* b = (const char*)(vbase + (int64_t)kt * a.v_st);
+        const int lim = kt + BN <= ke ? NTHREADS * T::V_LOADS : (ke - kt) * T::VGR;
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                float t = s[mb][i] * a.scale_log2;
-                if (need_mask) {
-                    const int kpos = kt + mb * 32 + (i >> 2) * 8 + lg * 4 + (i & 3);
-                    if (kpos > qpos || kpos >= ke) t = -INFINITY;
-                }
-                s[mb][i] = t;
-                mloc = fmaxf(mloc, t);
-            }
-        mloc = wave_swap32_max(mloc);
-        const float m_new = fmaxf(m_run, mloc);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-        m_run = m_new;
-
-        // P = exp2(t - m), its row sum, and P in bf16 as the B operand of O^T += V^T P^T
-        float psum = 0.f;
-        bf16x8 pb[2][2];
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const float p = __builtin_amdgcn_exp2f(s[mb][i] - m_use);
-                psum += p;
-                pb[mb][i >> 3][i & 7] = (__bf16)p;
-            }
-        l_run = l_run * alpha + psum;
-#pragma unroll
-        for (int d = 0; d < DB; ++d)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) o[d][i] *= alpha;
-
-#pragma unroll
-        for (int d = 0; d < DB; ++d) {
-            const u16* vrow = &sm.vt[(d * 32 + lr) * VT_STRIDE + lg * 4];
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                for (int hh = 0; hh < 2; ++hh) {
-                    const int ko = mb * 32 + hh * 16;
-                    const u32x2 lo = *(const u32x2*)(vrow + ko);
-                    const u32x2 hi = *(const u32x2*)(vrow + ko + 8);
-                    const u32x4 raw = {lo[0], lo[1], hi[0], hi[1]};
-                    o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, raw), pb[mb][hh], o[d], 0, 0, 0);
-                }
-        }
+        for (int t = 0; t < T::V_LOADS; ++t)
+            if (t * NTHREADS + tid < lim)
+                __builtin_amdgcn_global_load_lds((glb_void_t*)(b + v_src[t]),
+                                                 (lds_void_t*)(buf + (t * NWAVES + wave) * 1024), 16, 0, 0);
+    };
+    if (ntiles > 0) {
+        // zero both V buffers once, so rows a tail tile does not load are finite
+        for (int i = tid; i < 2 * T::V_BYTES / 16; i += NTHREADS)
+            *(u32x4*)(vbuf0 + i * 16) = u32x4{0u, 0u, 0u, 0u};
+        lds_barrier();
+        issue_k(kbuf0, kb);
+        issue_v(vbuf0, kb);
+        if (ntiles > 1) issue_k(kbuf0 + T::K_BYTES, kb + BN);
     }
 
-    // epilogue: normalise and store
-    const float l_tot = wave_swap32_add(l_run);
-    const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const float lse_val = l_tot > 0.f ? (m_run + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
-    if (!row_valid) return;
-    const int row = it.row0 + rloc;
-    if constexpr (SPLIT) {
-        float* po = a.part_o + (((int64_t)it.split * a.tokens + row) * a.num_heads + h) * DV;
+    const int wave_first = it.pos0 + wave * 64;
+
+    // Per-lane LDS byte offsets; the rest of each address is an immediate.
+    // K (A operand of S^T): row mb*32+lr, granule ks*2+lg, swizzled with lr&7.
+    int k_off[4];
 #pragma unroll
-        for (int d = 0; d < DB; ++d)
+    for (int r = 0; r < 4; ++r) k_off[r] = lr * (T::KGR * 16) + ((((r * 2) + lg) ^ (lr & 7)) * 16);
+    // V^T (A operand of O^T) through ds_read_b64_tr_b16: 16-lane group q reads
+    // keys 4*(q>>1) + (j>>2) and value columns 16*(q&1) + 4*(j&3) .. +3.
+    const int tq = lane >> 4, tj = lane & 15;
+    const int tr_key = 4 * (tq >> 1) + (tj >> 2);
+    const int tr_col = 16 * (tq & 1) + 4 * (tj & 3);
+    int v_off[2];
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                float4 w = {o[d][c * 4 + 0] * inv_l, o[d][c * 4 + 1] * inv_l,
-                            o[d][c * 4 + 2] * inv_l, o[d][c * 4 + 3] * inv_l};
-                *(float4*)(po + d * 32 + c * 8 + lg * 4) = w;
+    for (int r = 0; r < 2; ++r)
+        v_off[r] = tr_key * (T::VGR * 16) + ((((r * 4) + (tr_col >> 3)) ^ tr_key) * 16) + (tr_col & 7) * 2;
+
+    float m_run[2] = {-INFINITY, -INFINITY};  // max used by exp2 (log2 units), refreshed lazily
+    float l_part[2] = {0.f, 0.f};            // this lane's share of the softmax denominator
+    f32x16 o[DB][2];
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[d][nb][i] = 0.f;
+
+    auto load_kfrag = [&](const char* kt_buf, int ks, int mb) -> bf16x8 {
+        const u32x4 raw = *(const u32x4*)(kt_buf + mb * 32 * T::KGR * 16 + (ks >> 2) * 128 + k_off[ks & 3]);
+        return __builtin_bit_cast(bf16x8, raw);
+    };
+    auto load_vfrag = [&](const char* vt, int mb, int hh, int d) -> bf16x8 {
+        bf16x8 af;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const char* addr = vt + (mb * 32 + hh * 16 + half * 8) * T::VGR * 16 + (d >> 1) * 128 + v_off[d & 1];
+            const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(addr));
+            const bf16x4 rb = __builtin_bit_cast(bf16x4, r);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) af[half * 4 + j] = rb[j];
+        }
+        return af;
+    };
+
+    // S^T = K Q^T for a whole tile (prologue only: no softmax to overlap with)
+    auto qk_all = [&](const char* kt_buf, f32x16 (&s)[2][2]) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+                const bf16x8 af = load_kfrag(kt_buf, ks, mb);
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb) {
+                    const bf16x8 bq = qf[nb][ks];
+                    if (ks == 0) MFMA_32x32x16_INIT(s[mb][nb], af, bq);
+                    else MFMA_32x32x16_ACC(s[mb][nb], af, bq);
+                }
             }
-        if (lg == 0) a.part_lse[((int64_t)it.split * a.num_heads + h) * a.tokens + row] = lse_val;
-    } else {
-        u16* op = a.out + (int64_t)row * a.o_st + (int64_t)h * a.o_sh;
+    };
+
+    // One key tile: mask S(t) if needed, then the scheduled mix of S(t+1)
+    // MFMAs, the softmax of S(t) and the O^T += V^T P^T MFMAs of tile t.
+    auto step = [&](auto P, auto HAS_NEXT, int t, f32x16 (&s_cur)[2][2], f32x16 (&s_nxt)[2][2]) {
+        constexpr int par = decltype(P)::value;
+        constexpr bool has_next = decltype(HAS_NEXT)::value;
+        const char* kt_nxt = kbuf0 + (1 - par) * T::K_BYTES;
+        const char* vt_cur = vbuf0 + par * T::V_BYTES;
+        const int kt = kb + t * BN;
+        wait_vmcnt<0>();
+        lds_barrier();  // K(t+1), V(t) are in LDS; every wave is done with K(t) and V(t-1)
+        if (t + 2 < ntiles) issue_k(kbuf0 + par * T::K_BYTES, kt + 2 * BN);
+        if (has_next && t + 1 < ntiles) issue_v(vbuf0 + (1 - par) * T::V_BYTES, kt + BN);
+
+        // causal / range mask on the tiles that cross a row's last visible key:
+        // key kt + c (c = mb*32 + (i>>2)*8 + lg*4 + (i&3)) is hidden when
+        // c > qlim - kt, with qlim = min(row position, ke - 1) - lg*4
+        if ((kt + BN - 1 > wave_first) || (kt + BN > ke)) {
 #pragma unroll
-        for (int d = 0; d < DB; ++d)
+            for (int nb = 0; nb < 2; ++nb) {
+                const int lim = qlim[nb] - kt;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-                bf16x4 w;
+                for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][c * 4 + j] * inv_l);
-                *(bf16x4*)(op + d * 32 + c * 8 + lg * 4) = w;
+                    for (int i = 0; i < 16; ++i)
+                        if (mb * 32 + (i >> 2) * 8 + (i & 3) > lim) s_cur[mb][nb][i] = -INFINITY;
             }
-        if (lg == 0 && a.lse) a.lse[(int64_t)h * a.lse_sh + row] = lse_val;
+        }
+
+        float alpha[2] = {1.f, 1.f}, m_use[2] = {0.f, 0.f};
+        bool refresh[2] = {false, false};
+        float lsum[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
+        bf16x8 pb[2][2][2];          // [nb][mb][hh]
+        bf16x8 kf[2];                // K fragments, double-buffered in issue order
+        bf16x8 vf[2][DB];            // V^T fragments: [group & 1][d]
+
+        auto piece = [&](auto K) {
+            constexpr int k = decltype(K)::value;
+            if constexpr (k < 2) {
+                constexpr int nb = k;
+                float mx = -INFINITY;
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                    for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s_cur[mb][nb][i], s_cur[mb][nb][i + 1]));
+                mx = lane_swap32_max(mx) * a.scale_log2;
+                refresh[nb] = __builtin_amdgcn_ballot_w64(mx > m_run[nb] + LAZY_TAU) != 0;
+                const float m_new = refresh[nb] ? fmaxf(m_run[nb], mx) : m_run[nb];
+                // a row that has seen no visible key yet (m_new = -inf) has nothing to rescale
+                alpha[nb] = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
+                m_run[nb] = m_new;
+                m_use[nb] = (m_new == -INFINITY) ? 0.f : m_new;
+                l_part[nb] *= alpha[nb];
+            } else {
+                constexpr int u = (k - 2) >> 1, half = (k - 2) & 1;
+                constexpr int mb = u >> 2, hh = (u >> 1) & 1, nb = u & 1;
+#pragma unroll
+                for (int j = 0; j < 4; j += 2) {
+                    const int i = hh * 8 + half * 4 + j;
+                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mb][nb][i], a.scale_log2, -m_use[nb]));
+                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mb][nb][i + 1], a.scale_log2, -m_use[nb]));
+                    lsum[nb][0] += p0;
+                    lsum[nb][1] += p1;
+                    pb[nb][mb][hh][half * 4 + j] = (__bf16)p0;
+                    pb[nb][mb][hh][half * 4 + j + 1] = (__bf16)p1;
+                }
+            }
+        };
+
+        auto run = [&](auto tag) {
+            typedef typename decltype(tag)::type Sch;
+            constexpr Sch sch{};
+            constexpr int NS = Sch::NS;
+            // fragments needed first: V^T group 0, and K k-step 0 of the next tile
+            static_for<DB>([&](auto D) { vf[0][D] = load_vfrag(vt_cur, 0, 0, D); });
+            if constexpr (has_next) kf[0] = load_kfrag(kt_nxt, QkCoords<KS>::ks(0), QkCoords<KS>::mb(0));
+            static_for<NS>([&](auto SL) {
+                constexpr int s = SL;
+                constexpr int kind = sch.kind[s];
+                constexpr int idx = sch.index[s];
+                if constexpr (s == sch.rescale_before) {
+                    if (refresh[0] || refresh[1]) {
+                        // rare: rescale the AGPR accumulators 16 at a time, so the
+                        // branch needs only a few temporary VGPRs
+                        mfma_drain();
+                        static_for<2 * DB>([&](auto J) {
+                            constexpr int nb = J / DB, d = J % DB;
+                            scale_agpr_tile(o[d][nb], alpha[nb]);
+                            __builtin_amdgcn_sched_barrier(0);
+                        });
+                    }
+                }
+                if constexpr (kind == 2) {
+                    // VALU-only slot
+                } else if constexpr (kind == 0) {
+                    typedef QkCoords<KS> C;
+                    constexpr int ks = C::ks(idx), mb = C::mb(idx), nb = C::nb(idx);
+                    constexpr int frag = idx >> 1;  // (mb, ks) in issue order
+                    // prefetch the next (mb, ks) fragment with this one's first MFMA
+                    if constexpr (nb == 0 && frag + 1 < 2 * KS)
+                        kf[(frag + 1) & 1] = load_kfrag(kt_nxt, C::ks(2 * (frag + 1)), C::mb(2 * (frag + 1)));
+                    const bf16x8 af = kf[frag & 1];
+                    const bf16x8 bq = qf[nb][ks];
+                    if constexpr (ks == 0) MFMA_32x32x16_INIT(s_nxt[mb][nb], af, bq);
+                    else MFMA_32x32x16_ACC(s_nxt[mb][nb], af, bq);
+                } else {
+                    constexpr int unit = idx / DB, d = idx % DB;
+                    constexpr int mb = unit >> 2, hh = (unit >> 1) & 1, nb = unit & 1;
+                    constexpr int grp = unit >> 1;  // (mb, hh): shared by both query blocks
+                    // prefetch the next group's V^T fragments with this group's first MFMA
+                    if constexpr (nb == 0 && d == 0 && grp + 1 < 4) {
+                        static_for<DB>([&](auto D) {
+                            vf[(grp + 1) & 1][D] = load_vfrag(vt_cur, (grp + 1) >> 1, (grp + 1) & 1, D);
+                        });
+                    }
+                    o[d][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[grp & 1][d], pb[nb][mb][hh], o[d][nb], 0, 0, 0);
+                }
+                constexpr int p0 = s == 0 ? 0 : sch.pieces_end[s == 0 ? 0 : s - 1];
+                constexpr int p1 = sch.pieces_end[s];
+                static_for<N_PIECES>([&](auto K) {
+                    if constexpr (K >= p0 && K < p1) piece(K);
+                });
+                __builtin_amdgcn_sched_barrier(0);
+            });
+        };
+        if constexpr (has_next) run(std::type_identity<SchedFull>());
+        else run(std::type_identity<SchedLast>());
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) l_part[nb] += lsum[nb][0] + lsum[nb][1];
+    };
+
+    if (ntiles > 0) {
+        typedef std::integral_constant<int, 0> P0;
+        typedef std::integral_constant<int, 1> P1;
+        typedef std::integral_constant<bool, true> NX;
+        typedef std::integral_constant<bool, false> LAST;
+        f32x16 s_a[2][2], s_b[2][2];
+        wait_vmcnt<0>();
+        lds_barrier();
+        qk_all(kbuf0, s_a);
+        mfma_drain();
+        // Tiles in pairs (static buffer parity). With an even tile count the
+        // last pair computes one S^T tile too many, from stale LDS data, and
+        // discards it: cheaper than a third step variant's registers.
+        int t = 0;
+        for (; t + 1 < ntiles; t += 2) {
+            step(P0(), NX(), t, s_a, s_b);
+            step(P1(), NX(), t + 1, s_b, s_a);
+        }
+        if (t < ntiles) step(P0(), LAST(), t, s_a, s_b);
+        mfma_drain();
+    }
+
+    // ---- epilogue: normalise and store ----
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+        const float l_tot = lane_swap32_add(l_part[nb]);
+        const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        const float lse_val = l_tot > 0.f ? (m_run[nb] + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
+        if (!qvalid[nb]) continue;
+        const int row = it.row0 + wave * 64 + nb * 32 + lr;
+        if constexpr (SPLIT) {
+            float* po = a.part_o + (((int64_t)it.split * a.tokens + row) * a.num_heads + h) * DV;
+#pragma unroll
+            for (int d = 0; d < DB; ++d)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    float4 w = {o[d][nb][c * 4 + 0] * inv_l, o[d][nb][c * 4 + 1] * inv_l,
+                                o[d][nb][c * 4 + 2] * inv_l, o[d][nb][c * 4 + 3] * inv_l};
+                    *(float4*)(po + d * 32 + c * 8 + lg * 4) = w;
+                }
+            if (lg == 0) a.part_lse[((int64_t)it.split * a.num_heads + h) * a.tokens + row] = lse_val;
+        } else {
+            u16* op = a.out + (int64_t)row * a.o_st + (int64_t)h * a.o_sh;
+#pragma unroll
+            for (int d = 0; d < DB; ++d)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    bf16x4 w;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][nb][c * 4 + j] * inv_l);
+                    *(bf16x4*)(op + d * 32 + c * 8 + lg * 4) = w;
+                }
+            if (lg == 0 && a.lse) a.lse[(int64_t)h * a.lse_sh + row] = lse_val;
+        }
     }
 }
 
