@@ -58,6 +58,9 @@ typedef uint16_t u16;
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
+// Word 3 of a raw buffer resource (untyped 32-bit data, no swizzle).
+constexpr int BUFFER_RSRC_WORD3 = 0x00020000;
+
 typedef vpp_chunk_attn_work_item_t WorkItem;
 static_assert(sizeof(WorkItem) == 32, "work item layout");
 
@@ -66,11 +69,10 @@ struct AttnArgs {
     const u16* q;
     const u16* k;
     const u16* v;
-    u16* out;
-    float* lse;
-    float* part_o;    // split mode: [splits][tokens][Hq][DV] fp32
-    float* part_lse;  // split mode: [splits][Hq][tokens] fp32
-    int64_t q_st, q_sh, k_st, k_sh, v_st, v_sh, o_st, o_sh, lse_sh;
+    void* out;   // bf16 [tokens][Hq][DV]; split mode: fp32 partials [splits][tokens][Hq][DV]
+    float* lse;  // fp32, h*lse_sh + row (nullable); split mode: partials [splits][Hq][tokens]
+    // element strides (the host checks that they fit in 31 bits)
+    int32_t q_st, q_sh, k_st, k_sh, v_st, v_sh, o_st, o_sh, lse_sh;
     int32_t num_items;
     int32_t num_heads;
     int32_t group;     // Hq / Hkv
@@ -83,7 +85,24 @@ struct AttnArgs {
 // granule index XOR-swizzled with (row & 7): the 8 rows a ds_read_b128 (K) or
 // ds_read_b64_tr_b16 (V) touches in one cycle then fall in 8 different bank
 // groups.
+// K tiles are read by ds_read_b128 (8 lanes per LDS cycle read 8 consecutive
+// rows at one granule): XOR the granule with row & 7. V tiles are read by
+// ds_read_b64_tr_b16 (16 lanes per cycle read 4 consecutive rows x 32 bytes):
+// XOR with ((row & 3) << 1) | ((row >> 2) & 1), which moves each of the 4 rows'
+// 32-byte segments to a different bank group and still keeps 8 consecutive
+// rows on 8 different granules.
 __device__ __forceinline__ int swz(int row, int granule) { return granule ^ (row & 7); }
+__device__ __forceinline__ int vswz_key(int row) { return ((row & 3) << 1) | ((row >> 2) & 1); }
+__device__ __forceinline__ int vswz(int row, int granule) { return granule ^ vswz_key(row); }
+
+// max of three floats in one v_max3_f32. Written as asm because the
+// compiler's maxnum would first canonicalise every operand coming from an asm
+// MFMA (one more VALU op per score); the scores are never NaN.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
 
 __device__ __forceinline__ float lane_swap32_max(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -349,11 +368,21 @@ void attn_fwd_kernel(AttnArgs a) {
 
     int item_id, h;
     work_coords(a, item_id, h);
-    const WorkItem it = a.items[item_id];
+    // the work item is uniform: keep it in SGPRs (so buffer resources built
+    // from it are scalar too)
+    WorkItem it = a.items[item_id];
+    it.row0 = __builtin_amdgcn_readfirstlane(it.row0);
+    it.nrows = __builtin_amdgcn_readfirstlane(it.nrows);
+    it.pos0 = __builtin_amdgcn_readfirstlane(it.pos0);
+    it.key_begin = __builtin_amdgcn_readfirstlane(it.key_begin);
+    it.key_end = __builtin_amdgcn_readfirstlane(it.key_end);
+    it.split = __builtin_amdgcn_readfirstlane(it.split);
+    it.kv_base = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(it.kv_base >> 32)) << 32) |
+                           (uint32_t)__builtin_amdgcn_readfirstlane((int)it.kv_base));
     const int hk = h / a.group;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS bases stay scalar
     const int lr = lane & 31;
     const int lg = lane >> 5;
 
@@ -377,12 +406,13 @@ void attn_fwd_kernel(AttnArgs a) {
         load_q_agpr<KS>(qf[nb], qp);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const int wave_first = it.pos0 + wave * 64;
 
-    // Global->LDS copy of one tile: per-lane element offsets are fixed and the
-    // tile base kt*stride is wave-uniform. In the last tile, rows past the key
-    // range are not loaded: their LDS rows keep older, finite data (the V
-    // buffers are zeroed first), and they are masked to probability 0.
-    uint32_t k_src[T::K_LOADS], v_src[T::V_LOADS];  // byte offsets from the tile base
+    // Global->LDS copy of one tile through a buffer resource whose base is the
+    // tile's first key row and whose size ends at the last key of the range:
+    // rows past the range read as zeros (buffer range check), so the last tile
+    // needs no special case. Per-lane byte offsets are fixed for the kernel.
+    uint32_t k_src[T::K_LOADS], v_src[T::V_LOADS];
 #pragma unroll
     for (int t = 0; t < T::K_LOADS; ++t) {
         const int slot = t * NTHREADS + tid;
@@ -393,40 +423,31 @@ void attn_fwd_kernel(AttnArgs a) {
     for (int t = 0; t < T::V_LOADS; ++t) {
         const int slot = t * NTHREADS + tid;
         const int row = slot / T::VGR, gs = slot % T::VGR;
-        v_src[t] = (uint32_t)(row * (int)a.v_st + swz(row, gs) * 8) * 2u;
+        v_src[t] = (uint32_t)(row * (int)a.v_st + vswz(row, gs) * 8) * 2u;
     }
-    // Slot t*NTHREADS + tid of a tile holds row slot / GR: in the last tile it is
-    // loaded only when that row is inside the key range, i.e. when the slot index
-    // is below (ke - kt) * GR.
     auto issue_k = [&](char* buf, int kt) {
-        const char* b = (const char*)(kbase + (int64_t)kt * a.k_st);
-        const int lim = kt + BN <= ke ? NTHREADS * T::K_LOADS : (ke - kt) * T::KGR;
+        const int rows = min(BN, ke - kt);
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(kbase + (int64_t)kt * a.k_st), (short)0, rows * (int)a.k_st * 2, BUFFER_RSRC_WORD3);
 #pragma unroll
         for (int t = 0; t < T::K_LOADS; ++t)
-            if (t * NTHREADS + tid < lim)
-                __builtin_amdgcn_global_load_lds((glb_void_t*)(b + k_src[t]),
-                                                 (lds_void_t*)(buf + (t * NWAVES + wave) * 1024), 16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(buf + (t * NWAVES + wave) * 1024), 16,
+                                                     (int)k_src[t], 0, 0, 0);
     };
     auto issue_v = [&](char* buf, int kt) {
-        const char* b = (const char*)(vbase + (int64_t)kt * a.v_st);
-        const int lim = kt + BN <= ke ? NTHREADS * T::V_LOADS : (ke - kt) * T::VGR;
+        const int rows = min(BN, ke - kt);
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(vbase + (int64_t)kt * a.v_st), (short)0, rows * (int)a.v_st * 2, BUFFER_RSRC_WORD3);
 #pragma unroll
         for (int t = 0; t < T::V_LOADS; ++t)
-            if (t * NTHREADS + tid < lim)
-                __builtin_amdgcn_global_load_lds((glb_void_t*)(b + v_src[t]),
-                                                 (lds_void_t*)(buf + (t * NWAVES + wave) * 1024), 16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(buf + (t * NWAVES + wave) * 1024), 16,
+                                                     (int)v_src[t], 0, 0, 0);
     };
     if (ntiles > 0) {
-        // zero both V buffers once, so rows a tail tile does not load are finite
-        for (int i = tid; i < 2 * T::V_BYTES / 16; i += NTHREADS)
-            *(u32x4*)(vbuf0 + i * 16) = u32x4{0u, 0u, 0u, 0u};
-        lds_barrier();
         issue_k(kbuf0, kb);
         issue_v(vbuf0, kb);
         if (ntiles > 1) issue_k(kbuf0 + T::K_BYTES, kb + BN);
     }
-
-    const int wave_first = it.pos0 + wave * 64;
 
     // Per-lane LDS byte offsets; the rest of each address is an immediate.
     // K (A operand of S^T): row mb*32+lr, granule ks*2+lg, swizzled with lr&7.
@@ -441,7 +462,7 @@ void attn_fwd_kernel(AttnArgs a) {
     int v_off[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r)
-        v_off[r] = tr_key * (T::VGR * 16) + ((((r * 4) + (tr_col >> 3)) ^ tr_key) * 16) + (tr_col & 7) * 2;
+        v_off[r] = tr_key * (T::VGR * 16) + ((((r * 4) + (tr_col >> 3)) ^ vswz_key(tr_key)) * 16) + (tr_col & 7) * 2;
 
     float m_run[2] = {-INFINITY, -INFINITY};  // max used by exp2 (log2 units), refreshed lazily
     float l_part[2] = {0.f, 0.f};            // this lane's share of the softmax denominator
@@ -525,11 +546,15 @@ void attn_fwd_kernel(AttnArgs a) {
             constexpr int k = decltype(K)::value;
             if constexpr (k < 2) {
                 constexpr int nb = k;
-                float mx = -INFINITY;
+                // two independent max3 chains over the 32 scores of this query block
+                float mx0 = max3f(s_cur[0][nb][0], s_cur[0][nb][1], s_cur[0][nb][2]);
+                float mx1 = max3f(s_cur[1][nb][0], s_cur[1][nb][1], s_cur[1][nb][2]);
 #pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                    for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s_cur[mb][nb][i], s_cur[mb][nb][i + 1]));
+                for (int i = 3; i < 15; i += 2) {
+                    mx0 = max3f(mx0, s_cur[0][nb][i], s_cur[0][nb][i + 1]);
+                    mx1 = max3f(mx1, s_cur[1][nb][i], s_cur[1][nb][i + 1]);
+                }
+                float mx = max3f(mx0, mx1, max3f(s_cur[0][nb][15], s_cur[1][nb][15], -INFINITY));
                 mx = lane_swap32_max(mx) * a.scale_log2;
                 refresh[nb] = __builtin_amdgcn_ballot_w64(mx > m_run[nb] + LAZY_TAU) != 0;
                 const float m_new = refresh[nb] ? fmaxf(m_run[nb], mx) : m_run[nb];
@@ -647,7 +672,7 @@ void attn_fwd_kernel(AttnArgs a) {
         if (!qvalid[nb]) continue;
         const int row = it.row0 + wave * 64 + nb * 32 + lr;
         if constexpr (SPLIT) {
-            float* po = a.part_o + (((int64_t)it.split * a.tokens + row) * a.num_heads + h) * DV;
+            float* po = (float*)a.out + (((int64_t)it.split * a.tokens + row) * a.num_heads + h) * DV;
 #pragma unroll
             for (int d = 0; d < DB; ++d)
 #pragma unroll
@@ -656,9 +681,9 @@ void attn_fwd_kernel(AttnArgs a) {
                                 o[d][nb][c * 4 + 2] * inv_l, o[d][nb][c * 4 + 3] * inv_l};
                     *(float4*)(po + d * 32 + c * 8 + lg * 4) = w;
                 }
-            if (lg == 0) a.part_lse[((int64_t)it.split * a.num_heads + h) * a.tokens + row] = lse_val;
+            if (lg == 0) a.lse[((int64_t)it.split * a.num_heads + h) * a.tokens + row] = lse_val;
         } else {
-            u16* op = a.out + (int64_t)row * a.o_st + (int64_t)h * a.o_sh;
+            u16* op = (u16*)a.out + (int64_t)row * a.o_st + (int64_t)h * a.o_sh;
 #pragma unroll
             for (int d = 0; d < DB; ++d)
 #pragma unroll
@@ -971,6 +996,12 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
         !stride_ok(v_sh) || !stride_ok(o_st) || !stride_ok(o_sh))
         return VPP_ERR_INVALID_ARG;
     if (lse && (((uintptr_t)lse & 3u) != 0 || lse_sh < p->tokens)) return VPP_ERR_INVALID_ARG;
+    // the kernels keep element strides in 32 bits; a stride times the 64 rows of
+    // a tile must also stay below 2^31 for the buffer resources
+    const int64_t smax = ((int64_t)1 << 31) / 64;
+    if (q_st >= smax || q_sh >= smax || k_st >= smax || k_sh >= smax || v_st >= smax || v_sh >= smax ||
+        o_st >= smax || o_sh >= smax || (lse && lse_sh >= ((int64_t)1 << 31)))
+        return VPP_ERR_INVALID_ARG;
     if (!workspace || ((uintptr_t)workspace & 255u) != 0) return VPP_ERR_WORKSPACE;
     if (workspace_bytes < p->ws_bytes) return VPP_ERR_WORKSPACE;
     if (p->items.empty()) return VPP_OK;  // nothing to do: every segment is empty
@@ -1008,10 +1039,11 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
     a.q = (const u16*)q;
     a.k = (const u16*)k;
     a.v = (const u16*)v;
-    a.out = (u16*)out;
+    a.out = out;
     a.lse = lse;
-    a.q_st = q_st; a.q_sh = q_sh; a.k_st = k_st; a.k_sh = k_sh; a.v_st = v_st; a.v_sh = v_sh;
-    a.o_st = o_st; a.o_sh = o_sh; a.lse_sh = lse_sh;
+    a.q_st = (int32_t)q_st; a.q_sh = (int32_t)q_sh; a.k_st = (int32_t)k_st; a.k_sh = (int32_t)k_sh;
+    a.v_st = (int32_t)v_st; a.v_sh = (int32_t)v_sh; a.o_st = (int32_t)o_st; a.o_sh = (int32_t)o_sh;
+    a.lse_sh = (int32_t)lse_sh;
     a.num_items = (int32_t)p->items.size();
     a.num_heads = c.num_q_heads;
     a.group = c.num_q_heads / c.num_kv_heads;
@@ -1023,11 +1055,11 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
     memset(&ca, 0, sizeof ca);
     if (split) {
         size_t off = align256(p->items_bytes);
-        a.part_o = (float*)(ws + off);
+        ca.part_o = (float*)(ws + off);
         off += align256((size_t)p->num_splits * p->tokens * c.num_q_heads * c.head_dim_v * sizeof(float));
-        a.part_lse = (float*)(ws + off);
-        ca.part_o = a.part_o;
-        ca.part_lse = a.part_lse;
+        ca.part_lse = (float*)(ws + off);
+        a.out = (void*)ca.part_o;
+        a.lse = (float*)ca.part_lse;
         ca.out = (u16*)out;
         ca.lse = lse;
         ca.o_st = o_st; ca.o_sh = o_sh; ca.lse_sh = lse_sh;
