@@ -175,59 +175,64 @@ struct QkCoords {
 //
 // One wave (one SIMD) runs, per tile, NQK MFMAs of the next tile's S^T, NPV
 // MFMAs of this tile's O^T update and the softmax of this tile in fp32 VALU
-// code. A wave issues in order, and VALU work issued between two MFMAs runs
-// while the matrix core is busy, so the softmax is cut into pieces spread
-// evenly over the MFMA slots:
-//   piece 0, 1          row max of query block 0 / 1 (and the lazy rescale decision)
-//   piece 2 + 2u + h    exp, row sum and bf16 packing of 4 elements of unit u, half h
-// where unit u = (key block mb, 16-key group hh, query block nb) = (u>>2, (u>>1)&1, u&1)
-// holds the 8 P values one O^T MFMA group consumes. O^T MFMAs of unit u are
-// placed only after its two pieces; all pieces finish before the last unit's
-// MFMAs, which therefore run alone at the end of the tile.
+// code. A wave issues in order; VALU work issued right after an MFMA runs
+// while the matrix core is busy (about 5 VALU instructions fit under one
+// 32x32x16 MFMA), so the softmax is cut into small atoms spread evenly over
+// the MFMA slots:
+//   atoms 0..7     4 v_max3 steps of the row max (query block nb = a >> 2)
+//   atoms 8, 9     finish the row max of block 0 / 1: lane exchange, lazy
+//                  rescale decision, new reference max
+//   atoms 10..73   one score each: exp2, row sum, bf16 packing; element
+//                  e = a - 10 belongs to unit u = e >> 3, which holds the 8 P
+//                  values one O^T MFMA group consumes:
+//                  (key block mb, 16-key group hh, query block nb) = (u>>2, (u>>1)&1, u&1)
+// An O^T MFMA of unit u is placed only after the unit's 8 atoms; all atoms
+// finish before the last unit's MFMAs, which run alone at the end of the tile.
 // ---------------------------------------------------------------------------
-constexpr int N_PIECES = 18;
-constexpr int piece_weight(int k) { return k < 2 ? 140 : 92; }  // VALU cycles, measured rates
+constexpr int N_ATOMS = 74;
+constexpr int ATOM_MAXF = 8;   // first finishing atom
+constexpr int ATOM_EXP = 10;   // first exp atom
+constexpr int atom_weight(int k) { return k < ATOM_MAXF ? 24 : (k < ATOM_EXP ? 70 : 23); }  // VALU cycles
+constexpr int unit_last_atom(int u) { return ATOM_EXP + 8 * u + 7; }
 
 template <int NQK, int NPV, int DB>
 struct Schedule {
     // the last tile has no next S^T to overlap with: it opens with one
-    // VALU-only slot, then hides each unit's softmax under the previous unit's MFMAs
+    // VALU-only slot for the row max, then hides each unit's atoms under the
+    // previous unit's MFMAs
     static constexpr int NS = NQK + NPV + (NQK == 0 ? 1 : 0);
-    int kind[NS] = {};       // 0: S^T MFMA, 1: O^T MFMA, 2: no MFMA
-    int index[NS] = {};      // S^T: see qk_coords; O^T: unit*DB + d
-    int pieces_end[NS] = {}; // VALU pieces issued after this slot: [pieces_end[s-1], pieces_end[s])
-    int rescale_before = 0;  // slot before which the (rare) O rescale check runs
+    int kind[NS] = {};      // 0: S^T MFMA, 1: O^T MFMA, 2: no MFMA
+    int index[NS] = {};     // S^T: see QkCoords; O^T: unit*DB + d
+    int atoms_end[NS] = {}; // atoms issued after slot s: [atoms_end[s-1], atoms_end[s])
+    int rescale_before = 0; // slot before which the (rare) O rescale check runs
     constexpr Schedule() {
-        int done_at[N_PIECES] = {};
+        int done_at[N_ATOMS] = {};
         if constexpr (NQK == 0) {
             kind[0] = 2;
-            for (int k = 0; k < 4; ++k) done_at[k] = 0;
+            for (int k = 0; k < ATOM_EXP + 8; ++k) done_at[k] = 0;
             for (int p = 0; p < NPV; ++p) {
                 kind[1 + p] = 1;
                 index[1 + p] = p;
             }
-            for (int u = 1; u < 8; ++u) {  // unit u under unit u-1's MFMAs
-                const int first = 1 + (u - 1) * DB;
-                done_at[2 + 2 * u] = first;
-                done_at[3 + 2 * u] = first + (DB > 1 ? 1 : 0);
-            }
+            for (int u = 1; u < 8; ++u)  // unit u under unit u-1's MFMAs
+                for (int j = 0; j < 8; ++j) done_at[ATOM_EXP + 8 * u + j] = 1 + (u - 1) * DB + (j * DB) / 8;
         } else {
-            // slot by which each piece must be done: spread by weight over the
-            // slots before the last unit's MFMAs
+            // slot by which each atom is done: spread by weight over the slots
+            // before the last unit's MFMAs
             int total = 0;
-            for (int k = 0; k < N_PIECES; ++k) total += piece_weight(k);
+            for (int k = 0; k < N_ATOMS; ++k) total += atom_weight(k);
             const int span = NS - DB;
             int acc = 0;
-            for (int k = 0; k < N_PIECES; ++k) {
-                acc += piece_weight(k);
+            for (int k = 0; k < N_ATOMS; ++k) {
+                acc += atom_weight(k);
                 int s = (acc * span + total - 1) / total - 1;
                 done_at[k] = s < 0 ? 0 : s;
             }
-            // MFMA order: an O^T MFMA as soon as its unit's pieces are done, else an S^T MFMA
+            // MFMA order: an O^T MFMA as soon as its unit's atoms are done, else an S^T MFMA
             int q = 0, p = 0;
             for (int s = 0; s < NS; ++s) {
                 const int unit = p / DB;
-                const bool pv_ready = p < NPV && done_at[1] < s && done_at[2 + 2 * unit + 1] < s;
+                const bool pv_ready = p < NPV && done_at[ATOM_EXP - 1] < s && done_at[unit_last_atom(unit)] < s;
                 if (pv_ready || q >= NQK) {
                     kind[s] = 1;
                     index[s] = p++;
@@ -239,22 +244,23 @@ struct Schedule {
         }
         for (int s = 0; s < NS; ++s) {
             int n = 0;
-            for (int k = 0; k < N_PIECES; ++k) n += done_at[k] <= s;
-            pieces_end[s] = n;
+            for (int k = 0; k < N_ATOMS; ++k) n += done_at[k] <= s;
+            atoms_end[s] = n;
         }
         rescale_before = NS;
         for (int s = NS - 1; s >= 0; --s)
             if (kind[s] == 1) rescale_before = s;
     }
-    // every O^T MFMA comes after the pieces it depends on
+    // every O^T MFMA comes after the atoms it depends on; atoms run in order
     constexpr bool valid() const {
         for (int s = 0; s < NS; ++s) {
+            if (s > 0 && atoms_end[s] < atoms_end[s - 1]) return false;
             if (kind[s] != 1) continue;
             const int unit = index[s] / DB;
-            const int before = s == 0 ? 0 : pieces_end[s - 1];
-            if (before < 2 + 2 * unit + 2) return false;
+            const int before = s == 0 ? 0 : atoms_end[s - 1];
+            if (before < unit_last_atom(unit) + 1) return false;
         }
-        return pieces_end[NS - 1] == N_PIECES;
+        return atoms_end[NS - 1] == N_ATOMS;
     }
 };
 
@@ -537,44 +543,44 @@ void attn_fwd_kernel(AttnArgs a) {
 
         float alpha[2] = {1.f, 1.f}, m_use[2] = {0.f, 0.f};
         bool refresh[2] = {false, false};
+        float mx[2] = {-INFINITY, -INFINITY};
         float lsum[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
+        float pprev = 0.f;
         bf16x8 pb[2][2][2];          // [nb][mb][hh]
-        bf16x8 kf[2];                // K fragments, double-buffered in issue order
+        bf16x8 kf[3];                // K fragments, issue order, two in flight
         bf16x8 vf[2][DB];            // V^T fragments: [group & 1][d]
 
-        auto piece = [&](auto K) {
+        auto atom = [&](auto K) {
             constexpr int k = decltype(K)::value;
-            if constexpr (k < 2) {
-                constexpr int nb = k;
-                // two independent max3 chains over the 32 scores of this query block
-                float mx0 = max3f(s_cur[0][nb][0], s_cur[0][nb][1], s_cur[0][nb][2]);
-                float mx1 = max3f(s_cur[1][nb][0], s_cur[1][nb][1], s_cur[1][nb][2]);
+            if constexpr (k < ATOM_MAXF) {
+                // 4 max3 steps over 8 of the 32 scores of query block nb
+                constexpr int nb = k >> 2, q = k & 3;
 #pragma unroll
-                for (int i = 3; i < 15; i += 2) {
-                    mx0 = max3f(mx0, s_cur[0][nb][i], s_cur[0][nb][i + 1]);
-                    mx1 = max3f(mx1, s_cur[1][nb][i], s_cur[1][nb][i + 1]);
+                for (int j = 0; j < 8; j += 2) {
+                    const int v = q * 8 + j;  // score index in [mb*16 + i]
+                    mx[nb] = max3f(mx[nb], s_cur[v >> 4][nb][v & 15], s_cur[(v + 1) >> 4][nb][(v + 1) & 15]);
                 }
-                float mx = max3f(mx0, mx1, max3f(s_cur[0][nb][15], s_cur[1][nb][15], -INFINITY));
-                mx = lane_swap32_max(mx) * a.scale_log2;
-                refresh[nb] = __builtin_amdgcn_ballot_w64(mx > m_run[nb] + LAZY_TAU) != 0;
-                const float m_new = refresh[nb] ? fmaxf(m_run[nb], mx) : m_run[nb];
+            } else if constexpr (k < ATOM_EXP) {
+                constexpr int nb = k - ATOM_MAXF;
+                const float m = lane_swap32_max(mx[nb]) * a.scale_log2;
+                refresh[nb] = __builtin_amdgcn_ballot_w64(m > m_run[nb] + LAZY_TAU) != 0;
+                const float m_new = refresh[nb] ? fmaxf(m_run[nb], m) : m_run[nb];
                 // a row that has seen no visible key yet (m_new = -inf) has nothing to rescale
                 alpha[nb] = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
                 m_run[nb] = m_new;
                 m_use[nb] = (m_new == -INFINITY) ? 0.f : m_new;
                 l_part[nb] *= alpha[nb];
             } else {
-                constexpr int u = (k - 2) >> 1, half = (k - 2) & 1;
+                constexpr int e = k - ATOM_EXP;
+                constexpr int u = e >> 3, j = e & 7;
                 constexpr int mb = u >> 2, hh = (u >> 1) & 1, nb = u & 1;
-#pragma unroll
-                for (int j = 0; j < 4; j += 2) {
-                    const int i = hh * 8 + half * 4 + j;
-                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mb][nb][i], a.scale_log2, -m_use[nb]));
-                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mb][nb][i + 1], a.scale_log2, -m_use[nb]));
-                    lsum[nb][0] += p0;
-                    lsum[nb][1] += p1;
-                    pb[nb][mb][hh][half * 4 + j] = (__bf16)p0;
-                    pb[nb][mb][hh][half * 4 + j + 1] = (__bf16)p1;
+                const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mb][nb][hh * 8 + j], a.scale_log2, -m_use[nb]));
+                lsum[nb][j & 1] += pv;
+                if constexpr ((j & 1) == 0) {
+                    pprev = pv;
+                } else {
+                    pb[nb][mb][hh][j - 1] = (__bf16)pprev;
+                    pb[nb][mb][hh][j] = (__bf16)pv;
                 }
             }
         };
@@ -583,9 +589,13 @@ void attn_fwd_kernel(AttnArgs a) {
             typedef typename decltype(tag)::type Sch;
             constexpr Sch sch{};
             constexpr int NS = Sch::NS;
-            // fragments needed first: V^T group 0, and K k-step 0 of the next tile
+            typedef QkCoords<KS> C;
+            // fragments needed first: V^T group 0, and the first two K fragments of the next tile
             static_for<DB>([&](auto D) { vf[0][D] = load_vfrag(vt_cur, 0, 0, D); });
-            if constexpr (has_next) kf[0] = load_kfrag(kt_nxt, QkCoords<KS>::ks(0), QkCoords<KS>::mb(0));
+            if constexpr (has_next) {
+                kf[0] = load_kfrag(kt_nxt, C::ks(0), C::mb(0));
+                kf[1] = load_kfrag(kt_nxt, C::ks(2), C::mb(2));
+            }
             static_for<NS>([&](auto SL) {
                 constexpr int s = SL;
                 constexpr int kind = sch.kind[s];
@@ -605,13 +615,12 @@ void attn_fwd_kernel(AttnArgs a) {
                 if constexpr (kind == 2) {
                     // VALU-only slot
                 } else if constexpr (kind == 0) {
-                    typedef QkCoords<KS> C;
                     constexpr int ks = C::ks(idx), mb = C::mb(idx), nb = C::nb(idx);
                     constexpr int frag = idx >> 1;  // (mb, ks) in issue order
-                    // prefetch the next (mb, ks) fragment with this one's first MFMA
-                    if constexpr (nb == 0 && frag + 1 < 2 * KS)
-                        kf[(frag + 1) & 1] = load_kfrag(kt_nxt, C::ks(2 * (frag + 1)), C::mb(2 * (frag + 1)));
-                    const bf16x8 af = kf[frag & 1];
+                    // prefetch two fragments ahead with this fragment's first MFMA
+                    if constexpr (nb == 0 && frag + 2 < 2 * KS)
+                        kf[(frag + 2) % 3] = load_kfrag(kt_nxt, C::ks(2 * (frag + 2)), C::mb(2 * (frag + 2)));
+                    const bf16x8 af = kf[frag % 3];
                     const bf16x8 bq = qf[nb][ks];
                     if constexpr (ks == 0) MFMA_32x32x16_INIT(s_nxt[mb][nb], af, bq);
                     else MFMA_32x32x16_ACC(s_nxt[mb][nb], af, bq);
@@ -627,10 +636,10 @@ void attn_fwd_kernel(AttnArgs a) {
                     }
                     o[d][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[grp & 1][d], pb[nb][mb][hh], o[d][nb], 0, 0, 0);
                 }
-                constexpr int p0 = s == 0 ? 0 : sch.pieces_end[s == 0 ? 0 : s - 1];
-                constexpr int p1 = sch.pieces_end[s];
-                static_for<N_PIECES>([&](auto K) {
-                    if constexpr (K >= p0 && K < p1) piece(K);
+                constexpr int a0 = s == 0 ? 0 : sch.atoms_end[s == 0 ? 0 : s - 1];
+                constexpr int a1 = sch.atoms_end[s];
+                static_for<N_ATOMS>([&](auto K) {
+                    if constexpr (K >= a0 && K < a1) atom(K);
                 });
                 __builtin_amdgcn_sched_barrier(0);
             });
