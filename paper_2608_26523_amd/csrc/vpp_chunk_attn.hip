@@ -186,8 +186,10 @@ struct QkCoords {
 //                  e = a - 10 belongs to unit u = e >> 3, which holds the 8 P
 //                  values one O^T MFMA group consumes:
 //                  (key block mb, 16-key group hh, query block nb) = (u>>2, (u>>1)&1, u&1)
-// An O^T MFMA of unit u is placed only after the unit's 8 atoms; all atoms
-// finish before the last unit's MFMAs, which run alone at the end of the tile.
+// O^T MFMA p works on key group g = p / (2*DB) (units 2g, 2g+1), value block
+// d = (p / 2) % DB and query block nb = p % 2, so each V^T fragment feeds two
+// MFMAs in a row; it is placed only after both units' atoms. All atoms finish
+// before the last group's MFMAs start.
 // ---------------------------------------------------------------------------
 constexpr int N_ATOMS = 74;
 constexpr int ATOM_MAXF = 8;   // first finishing atom
@@ -202,7 +204,7 @@ struct Schedule {
     // previous unit's MFMAs
     static constexpr int NS = NQK + NPV + (NQK == 0 ? 1 : 0);
     int kind[NS] = {};      // 0: S^T MFMA, 1: O^T MFMA, 2: no MFMA
-    int index[NS] = {};     // S^T: see QkCoords; O^T: unit*DB + d
+    int index[NS] = {};     // S^T: see QkCoords; O^T: see PvCoords
     int atoms_end[NS] = {}; // atoms issued after slot s: [atoms_end[s-1], atoms_end[s])
     int rescale_before = 0; // slot before which the (rare) O rescale check runs
     constexpr Schedule() {
@@ -214,25 +216,25 @@ struct Schedule {
                 kind[1 + p] = 1;
                 index[1 + p] = p;
             }
-            for (int u = 1; u < 8; ++u)  // unit u under unit u-1's MFMAs
-                for (int j = 0; j < 8; ++j) done_at[ATOM_EXP + 8 * u + j] = 1 + (u - 1) * DB + (j * DB) / 8;
+            for (int g = 1; g < 4; ++g)  // key group g (units 2g, 2g+1) under group g-1's MFMAs
+                for (int j = 0; j < 16; ++j) done_at[ATOM_EXP + 16 * g + j] = 1 + (g - 1) * 2 * DB + (j * 2 * DB) / 16;
         } else {
             // slot by which each atom is done: spread by weight over the slots
             // before the last unit's MFMAs
             int total = 0;
             for (int k = 0; k < N_ATOMS; ++k) total += atom_weight(k);
-            const int span = NS - DB;
+            const int span = NS - 2 * DB;
             int acc = 0;
             for (int k = 0; k < N_ATOMS; ++k) {
                 acc += atom_weight(k);
                 int s = (acc * span + total - 1) / total - 1;
                 done_at[k] = s < 0 ? 0 : s;
             }
-            // MFMA order: an O^T MFMA as soon as its unit's atoms are done, else an S^T MFMA
+            // MFMA order: an O^T MFMA as soon as its key group's atoms are done, else an S^T MFMA
             int q = 0, p = 0;
             for (int s = 0; s < NS; ++s) {
-                const int unit = p / DB;
-                const bool pv_ready = p < NPV && done_at[ATOM_EXP - 1] < s && done_at[unit_last_atom(unit)] < s;
+                const int grp = p / (2 * DB);
+                const bool pv_ready = p < NPV && done_at[ATOM_EXP - 1] < s && done_at[unit_last_atom(2 * grp + 1)] < s;
                 if (pv_ready || q >= NQK) {
                     kind[s] = 1;
                     index[s] = p++;
@@ -256,9 +258,9 @@ struct Schedule {
         for (int s = 0; s < NS; ++s) {
             if (s > 0 && atoms_end[s] < atoms_end[s - 1]) return false;
             if (kind[s] != 1) continue;
-            const int unit = index[s] / DB;
+            const int grp = index[s] / (2 * DB);
             const int before = s == 0 ? 0 : atoms_end[s - 1];
-            if (before < unit_last_atom(unit) + 1) return false;
+            if (before < unit_last_atom(2 * grp + 1) + 1) return false;
         }
         return atoms_end[NS - 1] == N_ATOMS;
     }
@@ -547,8 +549,8 @@ void attn_fwd_kernel(AttnArgs a) {
         float lsum[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
         float pprev = 0.f;
         bf16x8 pb[2][2][2];          // [nb][mb][hh]
-        bf16x8 kf[3];                // K fragments, issue order, two in flight
-        bf16x8 vf[2][DB];            // V^T fragments: [group & 1][d]
+        bf16x8 kf[4];                // K fragments in issue order, three in flight
+        bf16x8 vf[3];                // V^T fragments in issue order, two in flight
 
         auto atom = [&](auto K) {
             constexpr int k = decltype(K)::value;
@@ -590,11 +592,13 @@ void attn_fwd_kernel(AttnArgs a) {
             constexpr Sch sch{};
             constexpr int NS = Sch::NS;
             typedef QkCoords<KS> C;
-            // fragments needed first: V^T group 0, and the first two K fragments of the next tile
-            static_for<DB>([&](auto D) { vf[0][D] = load_vfrag(vt_cur, 0, 0, D); });
+            // fragments needed first: two V^T fragments, and three K fragments of the next tile
+            vf[0] = load_vfrag(vt_cur, 0, 0, 0);
+            vf[1] = load_vfrag(vt_cur, 0, 0, 1 % DB);
             if constexpr (has_next) {
                 kf[0] = load_kfrag(kt_nxt, C::ks(0), C::mb(0));
                 kf[1] = load_kfrag(kt_nxt, C::ks(2), C::mb(2));
+                kf[2] = load_kfrag(kt_nxt, C::ks(4), C::mb(4));
             }
             static_for<NS>([&](auto SL) {
                 constexpr int s = SL;
@@ -617,24 +621,23 @@ void attn_fwd_kernel(AttnArgs a) {
                 } else if constexpr (kind == 0) {
                     constexpr int ks = C::ks(idx), mb = C::mb(idx), nb = C::nb(idx);
                     constexpr int frag = idx >> 1;  // (mb, ks) in issue order
-                    // prefetch two fragments ahead with this fragment's first MFMA
-                    if constexpr (nb == 0 && frag + 2 < 2 * KS)
-                        kf[(frag + 2) % 3] = load_kfrag(kt_nxt, C::ks(2 * (frag + 2)), C::mb(2 * (frag + 2)));
-                    const bf16x8 af = kf[frag % 3];
+                    // prefetch three fragments ahead with this fragment's first MFMA
+                    if constexpr (nb == 0 && frag + 3 < 2 * KS)
+                        kf[(frag + 3) % 4] = load_kfrag(kt_nxt, C::ks(2 * (frag + 3)), C::mb(2 * (frag + 3)));
+                    const bf16x8 af = kf[frag % 4];
                     const bf16x8 bq = qf[nb][ks];
                     if constexpr (ks == 0) MFMA_32x32x16_INIT(s_nxt[mb][nb], af, bq);
                     else MFMA_32x32x16_ACC(s_nxt[mb][nb], af, bq);
                 } else {
-                    constexpr int unit = idx / DB, d = idx % DB;
-                    constexpr int mb = unit >> 2, hh = (unit >> 1) & 1, nb = unit & 1;
-                    constexpr int grp = unit >> 1;  // (mb, hh): shared by both query blocks
-                    // prefetch the next group's V^T fragments with this group's first MFMA
-                    if constexpr (nb == 0 && d == 0 && grp + 1 < 4) {
-                        static_for<DB>([&](auto D) {
-                            vf[(grp + 1) & 1][D] = load_vfrag(vt_cur, (grp + 1) >> 1, (grp + 1) & 1, D);
-                        });
+                    constexpr int grp = idx / (2 * DB), d = (idx >> 1) % DB, nb = idx & 1;
+                    constexpr int mb = grp >> 1, hh = grp & 1;
+                    constexpr int frag = idx >> 1;  // (grp, d) in issue order
+                    // prefetch two fragments ahead with this fragment's first MFMA
+                    if constexpr (nb == 0 && frag + 2 < 4 * DB) {
+                        constexpr int f2 = frag + 2;
+                        vf[f2 % 3] = load_vfrag(vt_cur, (f2 / DB) >> 1, (f2 / DB) & 1, f2 % DB);
                     }
-                    o[d][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[grp & 1][d], pb[nb][mb][hh], o[d][nb], 0, 0, 0);
+                    o[d][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[frag % 3], pb[nb][mb][hh], o[d][nb], 0, 0, 0);
                 }
                 constexpr int a0 = s == 0 ? 0 : sch.atoms_end[s == 0 ? 0 : s - 1];
                 constexpr int a1 = sch.atoms_end[s];
