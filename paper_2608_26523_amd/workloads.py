@@ -151,16 +151,22 @@ def _slab_seed(seed: int, index: int, tensor: str, slab: int) -> int:
 
 
 def normal_bf16(shape, std: float, seed: int, index: int, tensor: str, device,
-                out=None):
-    """bf16 tensor of N(0,1)*std values, drawn slab by slab along dim 0."""
+                out=None, first_token: int = 0):
+    """bf16 tensor of N(0,1)*std values, drawn slab by slab along dim 0.
+
+    Row r of the result is token ``first_token + r`` of the full stream, which
+    must start on a slab boundary; the bits do not depend on ``first_token``.
+    """
     import torch
+    if first_token % SLAB_TOKENS:
+        raise ValueError("first_token must be a multiple of %d" % SLAB_TOKENS)
     if out is None:
         out = torch.empty(shape, dtype=torch.bfloat16, device=device)
     n = out.shape[0]
     gen = torch.Generator(device=out.device)
-    for slab, t0 in enumerate(range(0, n, SLAB_TOKENS)):
+    for t0 in range(0, n, SLAB_TOKENS):
         t1 = min(n, t0 + SLAB_TOKENS)
-        gen.manual_seed(_slab_seed(seed, index, tensor, slab))
+        gen.manual_seed(_slab_seed(seed, index, tensor, (first_token + t0) // SLAB_TOKENS))
         tmp = torch.randn((t1 - t0,) + tuple(out.shape[1:]), generator=gen,
                           device=out.device, dtype=torch.float32)
         out[t0:t1].copy_(tmp.mul_(std))
@@ -180,3 +186,12 @@ def make_inputs(w: Workload, device, tokens: int = 0):
     k = normal_bf16((s, w.hkv, w.dqk), std, w.seed, w.index, "k", device)
     v = normal_bf16((s, w.hkv, w.dv), std, w.seed, w.index, "v", device)
     return q, k, v
+
+
+def make_q_rows(w: Workload, device, t0: int, t1: int):
+    """Rows t0..t1-1 of the workload's q, the same bits as make_inputs (a view into
+    the enclosing slabs when t0 is not on a slab boundary)."""
+    std = 1.0 / math.sqrt(w.dqk)
+    a = t0 - t0 % SLAB_TOKENS
+    full = normal_bf16((t1 - a, w.hq, w.dqk), std, w.seed, w.index, "q", device, first_token=a)
+    return full[t0 - a:]
