@@ -71,6 +71,28 @@ def fit_line(xs, ys):
     return {"a_ms": a, "b_ms": b, "b_over_a": (b / a) if a else None, "r2": r2}
 
 
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_26523_amd", "csrc", "vpp_chunk_attn.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_fwd_hbm_bytes.md")
+
+
+def measured_traffic(workload):
+    """HBM bytes per attention launch from the committed FETCH_SIZE/WRITE_SIZE summary,
+    scaled by the copy-kernel factors; None unless the summary was taken on the kernel
+    source that is here now."""
+    import hashlib
+    try:
+        with open(KERNEL_SRC, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()[:16]
+        with open(TRAFFIC_FILE) as f:
+            for ln in f:
+                parts = ln.split()
+                if len(parts) == 4 and parts[0] == "traffic" and parts[1] == workload:
+                    return float(parts[3]) if parts[2] == sha else None
+    except OSError:
+        return None
+    return None
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -228,7 +250,7 @@ def main():
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None,
+                     "traffic": measured_traffic(w.name),
                      "kernel": "attn_fwd_kernel", "avg_launch_ms": round(kernel_ms, 4),
                      "flops_per_launch": total_flops / nchunks,
                      "algorithmic_bytes_per_launch": sum(nbytes) / nchunks},
