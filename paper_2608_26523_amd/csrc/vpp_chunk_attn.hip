@@ -359,6 +359,15 @@ template <int N, typename F>
 __device__ __forceinline__ void static_for(F&& f) {
     static_for_impl<N>(f, std::make_integer_sequence<int, N>());
 }
+// f(A0), f(A0 + 1), ..., f(A1 - 1)
+template <int A0, typename F, int... I>
+__device__ __forceinline__ void static_range_impl(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, A0 + I>()), ...);
+}
+template <int A0, int A1, typename F>
+__device__ __forceinline__ void static_range(F&& f) {
+    static_range_impl<A0>(f, std::make_integer_sequence<int, A1 - A0>());
+}
 
 template <int DQK, int DV, bool SPLIT>
 __global__ __attribute__((amdgpu_flat_work_group_size(NTHREADS, NTHREADS), amdgpu_waves_per_eu(1, 1)))
@@ -641,9 +650,7 @@ void attn_fwd_kernel(AttnArgs a) {
                 }
                 constexpr int a0 = s == 0 ? 0 : sch.atoms_end[s == 0 ? 0 : s - 1];
                 constexpr int a1 = sch.atoms_end[s];
-                static_for<N_ATOMS>([&](auto K) {
-                    if constexpr (K >= a0 && K < a1) atom(K);
-                });
+                static_range<a0, a1>([&](auto K) { atom(K); });
                 __builtin_amdgcn_sched_barrier(0);
             });
         };
