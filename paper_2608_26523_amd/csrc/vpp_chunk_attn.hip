@@ -46,6 +46,9 @@ constexpr int STAGING_SLOTS = 4;
 // max grows past it by more than this many powers of two; O and l share the
 // stale max, so the final quotient is unchanged and P stays <= 2^TAU.
 constexpr float LAZY_TAU = 8.0f;
+// The next tiles' global->LDS copies are spread over the first 1/LOAD_SPREAD
+// of a tile's MFMA slots.
+constexpr int LOAD_SPREAD = 2;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -60,6 +63,31 @@ typedef __attribute__((address_space(1))) void glb_void_t;
 
 // Word 3 of a raw buffer resource (untyped 32-bit data, no swizzle).
 constexpr int BUFFER_RSRC_WORD3 = 0x00020000;
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer resource over [base, base + bytes): reads past the end return 0.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, int32_t bytes) {
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)b);
+    r[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(b >> 32) & 0xffffu));  // stride 0
+    r[2] = __builtin_amdgcn_readfirstlane(bytes);
+    r[3] = BUFFER_RSRC_WORD3;
+    return r;
+}
+
+// 16 bytes per lane from global memory (resource + per-lane byte offset)
+// straight into LDS at lds_addr + 16*lane. Written as inline asm on purpose:
+// the compiler then does not track these copies as pending LDS writes and
+// inserts no wait for them in front of later LDS reads of other buffers; the
+// kernel waits for them itself (vmcnt) before the barrier that publishes the
+// buffer they fill. Nothing else in the kernel keeps a value in M0.
+__device__ __forceinline__ void copy16_to_lds(const i32x4& rsrc, uint32_t lds_addr, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds_addr), "v"(voff), "s"(rsrc)
+                 : "memory");
+}
 
 typedef vpp_chunk_attn_work_item_t WorkItem;
 static_assert(sizeof(WorkItem) == 32, "work item layout");
@@ -442,23 +470,24 @@ void attn_fwd_kernel(AttnArgs a) {
         const int row = slot / T::VGR, gs = slot % T::VGR;
         v_src[t] = (uint32_t)(row * (int)a.v_st + vswz(row, gs) * 8) * 2u;
     }
+    auto k_rsrc = [&](int kt) { return make_rsrc(kbase + (int64_t)kt * a.k_st, min(BN, ke - kt) * (int)a.k_st * 2); };
+    auto v_rsrc = [&](int kt) { return make_rsrc(vbase + (int64_t)kt * a.v_st, min(BN, ke - kt) * (int)a.v_st * 2); };
+    const uint32_t lds_wave = (uint32_t)(uintptr_t)(lds_void_t*)smem + (uint32_t)wave * 1024u;
+    auto load_k = [&](const i32x4& r, char* buf, int t) {
+        copy16_to_lds(r, lds_wave + (uint32_t)(buf - smem) + (uint32_t)(t * NWAVES * 1024), k_src[t]);
+    };
+    auto load_v = [&](const i32x4& r, char* buf, int t) {
+        copy16_to_lds(r, lds_wave + (uint32_t)(buf - smem) + (uint32_t)(t * NWAVES * 1024), v_src[t]);
+    };
     auto issue_k = [&](char* buf, int kt) {
-        const int rows = min(BN, ke - kt);
-        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(kbase + (int64_t)kt * a.k_st), (short)0, rows * (int)a.k_st * 2, BUFFER_RSRC_WORD3);
+        const i32x4 r = k_rsrc(kt);
 #pragma unroll
-        for (int t = 0; t < T::K_LOADS; ++t)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(buf + (t * NWAVES + wave) * 1024), 16,
-                                                     (int)k_src[t], 0, 0, 0);
+        for (int t = 0; t < T::K_LOADS; ++t) load_k(r, buf, t);
     };
     auto issue_v = [&](char* buf, int kt) {
-        const int rows = min(BN, ke - kt);
-        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(vbase + (int64_t)kt * a.v_st), (short)0, rows * (int)a.v_st * 2, BUFFER_RSRC_WORD3);
+        const i32x4 r = v_rsrc(kt);
 #pragma unroll
-        for (int t = 0; t < T::V_LOADS; ++t)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(buf + (t * NWAVES + wave) * 1024), 16,
-                                                     (int)v_src[t], 0, 0, 0);
+        for (int t = 0; t < T::V_LOADS; ++t) load_v(r, buf, t);
     };
     if (ntiles > 0) {
         issue_k(kbuf0, kb);
@@ -534,8 +563,12 @@ void attn_fwd_kernel(AttnArgs a) {
         const int kt = kb + t * BN;
         wait_vmcnt<0>();
         lds_barrier();  // K(t+1), V(t) are in LDS; every wave is done with K(t) and V(t-1)
-        if (t + 2 < ntiles) issue_k(kbuf0 + par * T::K_BYTES, kt + 2 * BN);
-        if (has_next && t + 1 < ntiles) issue_v(vbuf0 + (1 - par) * T::V_BYTES, kt + BN);
+        // the next tiles' copies (K(t+2) into the K buffer just freed, V(t+1)
+        // into the V buffer just freed) are spread over the first slots
+        const bool do_k = t + 2 < ntiles;
+        const bool do_v = has_next && t + 1 < ntiles;
+        const i32x4 rk = k_rsrc(do_k ? kt + 2 * BN : kb);
+        const i32x4 rv = v_rsrc(do_v ? kt + BN : kb);
 
         // causal / range mask on the tiles that cross a row's last visible key:
         // key kt + c (c = mb*32 + (i>>2)*8 + lg*4 + (i&3)) is hidden when
@@ -623,6 +656,18 @@ void attn_fwd_kernel(AttnArgs a) {
                             scale_agpr_tile(o[d][nb], alpha[nb]);
                             __builtin_amdgcn_sched_barrier(0);
                         });
+                    }
+                }
+                if constexpr (has_next) {
+                    constexpr int NL = T::K_LOADS + T::V_LOADS;
+                    constexpr int LSTRIDE = (NS / LOAD_SPREAD) / NL > 0 ? (NS / LOAD_SPREAD) / NL : 1;
+                    if constexpr (s % LSTRIDE == 0 && s / LSTRIDE < NL) {
+                        constexpr int j = s / LSTRIDE;
+                        if constexpr (j < T::V_LOADS) {
+                            if (do_v) load_v(rv, vbuf0 + (1 - par) * T::V_BYTES, j);
+                        } else {
+                            if (do_k) load_k(rk, kbuf0 + par * T::K_BYTES, j - T::V_LOADS);
+                        }
                     }
                 }
                 if constexpr (kind == 2) {
