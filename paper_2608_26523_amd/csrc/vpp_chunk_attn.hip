@@ -82,10 +82,12 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, int32_t bytes) {
 // inserts no wait for them in front of later LDS reads of other buffers; the
 // kernel waits for them itself (vmcnt) before the barrier that publishes the
 // buffer they fill. Nothing else in the kernel keeps a value in M0.
-__device__ __forceinline__ void copy16_to_lds(const i32x4& rsrc, uint32_t lds_addr, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+template <int OFF>
+__device__ __forceinline__ void copy16_to_lds(const i32x4& rsrc, uint32_t lds_base, uint32_t voff) {
+    // M0 = lds_base + OFF: one live SGPR for every copy of the kernel
+    asm volatile("s_add_u32 m0, %0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                  :
-                 : "s"(lds_addr), "v"(voff), "s"(rsrc)
+                 : "s"(lds_base), "v"(voff), "s"(rsrc), "i"(OFF)
                  : "memory");
 }
 
@@ -110,18 +112,30 @@ struct AttnArgs {
 };
 
 // LDS tiles: K [BN][DQK] and V [BN][DV] bf16, row-major in 16-byte granules,
-// granule index XOR-swizzled with (row & 7): the 8 rows a ds_read_b128 (K) or
-// ds_read_b64_tr_b16 (V) touches in one cycle then fall in 8 different bank
-// groups.
-// K tiles are read by ds_read_b128 (8 lanes per LDS cycle read 8 consecutive
-// rows at one granule): XOR the granule with row & 7. V tiles are read by
-// ds_read_b64_tr_b16 (16 lanes per cycle read 4 consecutive rows x 32 bytes):
-// XOR with ((row & 3) << 1) | ((row >> 2) & 1), which moves each of the 4 rows'
-// 32-byte segments to a different bank group and still keeps 8 consecutive
-// rows on 8 different granules.
-__device__ __forceinline__ int swz(int row, int granule) { return granule ^ (row & 7); }
-__device__ __forceinline__ int vswz_key(int row) { return ((row & 3) << 1) | ((row >> 2) & 1); }
-__device__ __forceinline__ int vswz(int row, int granule) { return granule ^ vswz_key(row); }
+// the granule index XOR-swizzled per row. The LDS serves 64 banks (256 bytes)
+// per cycle:
+//  * K is read by ds_read_b128, 16 lanes per cycle = 16 consecutive rows at one
+//    logical granule; the 16 granules must fall on 16 different 16-byte bank
+//    groups. With a multiple of 16 granules per row every row starts on the
+//    same bank, so XOR with row & 15; with 8 (mod 16) granules per row
+//    consecutive rows already alternate between the two 128-byte halves, so XOR
+//    with (row >> 1) & 7 within each half.
+//  * V is read by ds_read_b64_tr_b16, 32 lanes per cycle = 4 consecutive keys x
+//    64 bytes; the four segments must fall in four different 64-byte quarters:
+//    XOR with (key & 3) << 2 (16 granules per row), or with ((key >> 1) & 1) << 2
+//    (8 granules per row, where odd keys already sit in the other half).
+template <int KGR>
+__device__ __forceinline__ int kswz(int row, int granule) {
+    if constexpr (KGR % 16 == 0) return granule ^ (row & 15);
+    else return granule ^ ((row >> 1) & 7);
+}
+template <int VGR>
+__device__ __forceinline__ int vswz_bits(int key) {
+    if constexpr (VGR % 16 == 0) return (key & 3) << 2;
+    else return ((key >> 1) & 1) << 2;
+}
+template <int VGR>
+__device__ __forceinline__ int vswz(int key, int granule) { return granule ^ vswz_bits<VGR>(key); }
 
 // max of three floats in one v_max3_f32. Written as asm because the
 // compiler's maxnum would first canonicalise every operand coming from an asm
@@ -462,53 +476,64 @@ void attn_fwd_kernel(AttnArgs a) {
     for (int t = 0; t < T::K_LOADS; ++t) {
         const int slot = t * NTHREADS + tid;
         const int row = slot / T::KGR, gs = slot % T::KGR;
-        k_src[t] = (uint32_t)(row * (int)a.k_st + swz(row, gs) * 8) * 2u;
+        k_src[t] = (uint32_t)(row * (int)a.k_st + kswz<T::KGR>(row, gs) * 8) * 2u;
     }
 #pragma unroll
     for (int t = 0; t < T::V_LOADS; ++t) {
         const int slot = t * NTHREADS + tid;
         const int row = slot / T::VGR, gs = slot % T::VGR;
-        v_src[t] = (uint32_t)(row * (int)a.v_st + vswz(row, gs) * 8) * 2u;
+        v_src[t] = (uint32_t)(row * (int)a.v_st + vswz<T::VGR>(row, gs) * 8) * 2u;
     }
-    auto k_rsrc = [&](int kt) { return make_rsrc(kbase + (int64_t)kt * a.k_st, min(BN, ke - kt) * (int)a.k_st * 2); };
-    auto v_rsrc = [&](int kt) { return make_rsrc(vbase + (int64_t)kt * a.v_st, min(BN, ke - kt) * (int)a.v_st * 2); };
+    // resources over the rows [kt, min(kt + BN, ke)) (none when kt >= ke)
+    auto k_rsrc = [&](int kt) {
+        return make_rsrc(kbase + (int64_t)kt * a.k_st, max(0, min(BN, ke - kt)) * (int)a.k_st * 2);
+    };
+    auto v_rsrc = [&](int kt) {
+        return make_rsrc(vbase + (int64_t)kt * a.v_st, max(0, min(BN, ke - kt)) * (int)a.v_st * 2);
+    };
     const uint32_t lds_wave = (uint32_t)(uintptr_t)(lds_void_t*)smem + (uint32_t)wave * 1024u;
-    auto load_k = [&](const i32x4& r, char* buf, int t) {
-        copy16_to_lds(r, lds_wave + (uint32_t)(buf - smem) + (uint32_t)(t * NWAVES * 1024), k_src[t]);
+    // copy t of the K (V) tile into buffer B: LDS offset from this wave's base
+    auto load_k = [&](const i32x4& r, auto B, auto TT) {
+        constexpr int off = decltype(B)::value * T::K_BYTES + decltype(TT)::value * NWAVES * 1024;
+        copy16_to_lds<off>(r, lds_wave, k_src[decltype(TT)::value]);
     };
-    auto load_v = [&](const i32x4& r, char* buf, int t) {
-        copy16_to_lds(r, lds_wave + (uint32_t)(buf - smem) + (uint32_t)(t * NWAVES * 1024), v_src[t]);
+    auto load_v = [&](const i32x4& r, auto B, auto TT) {
+        constexpr int off = 2 * T::K_BYTES + decltype(B)::value * T::V_BYTES + decltype(TT)::value * NWAVES * 1024;
+        copy16_to_lds<off>(r, lds_wave, v_src[decltype(TT)::value]);
     };
-    auto issue_k = [&](char* buf, int kt) {
+    auto issue_k = [&](auto B, int kt) {
         const i32x4 r = k_rsrc(kt);
-#pragma unroll
-        for (int t = 0; t < T::K_LOADS; ++t) load_k(r, buf, t);
+        static_for<T::K_LOADS>([&](auto TT) { load_k(r, B, TT); });
     };
-    auto issue_v = [&](char* buf, int kt) {
+    auto issue_v = [&](auto B, int kt) {
         const i32x4 r = v_rsrc(kt);
-#pragma unroll
-        for (int t = 0; t < T::V_LOADS; ++t) load_v(r, buf, t);
+        static_for<T::V_LOADS>([&](auto TT) { load_v(r, B, TT); });
     };
     if (ntiles > 0) {
-        issue_k(kbuf0, kb);
-        issue_v(vbuf0, kb);
-        if (ntiles > 1) issue_k(kbuf0 + T::K_BYTES, kb + BN);
+        issue_k(std::integral_constant<int, 0>(), kb);
+        issue_v(std::integral_constant<int, 0>(), kb);
+        if (ntiles > 1) issue_k(std::integral_constant<int, 1>(), kb + BN);
     }
 
     // Per-lane LDS byte offsets; the rest of each address is an immediate.
-    // K (A operand of S^T): row mb*32+lr, granule ks*2+lg, swizzled with lr&7.
-    int k_off[4];
+    // K (A operand of S^T): row mb*32+lr, logical granule ks*2+lg; row & 15 and
+    // (row >> 1) & 7 depend only on lr. The swizzle touches the low 4 (or 3)
+    // bits of the granule index, so K_OFFS offsets cover every ks and the
+    // higher granule bits are an immediate.
+    constexpr int K_OFFS = (T::KGR % 16 == 0) ? 8 : 4;
+    int k_off[K_OFFS];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) k_off[r] = lr * (T::KGR * 16) + ((((r * 2) + lg) ^ (lr & 7)) * 16);
+    for (int r = 0; r < K_OFFS; ++r) k_off[r] = lr * (T::KGR * 16) + kswz<T::KGR>(lr, r * 2 + lg) * 16;
     // V^T (A operand of O^T) through ds_read_b64_tr_b16: 16-lane group q reads
-    // keys 4*(q>>1) + (j>>2) and value columns 16*(q&1) + 4*(j&3) .. +3.
+    // keys 4*(q>>1) + (j>>2) and value columns 16*(q&1) + 4*(j&3) .. +3, i.e.
+    // granule 4*d + (tr_col >> 3) of value block d; key & 3 = tr_key & 3.
     const int tq = lane >> 4, tj = lane & 15;
     const int tr_key = 4 * (tq >> 1) + (tj >> 2);
     const int tr_col = 16 * (tq & 1) + 4 * (tj & 3);
-    int v_off[2];
+    int v_off[DB];
 #pragma unroll
-    for (int r = 0; r < 2; ++r)
-        v_off[r] = tr_key * (T::VGR * 16) + ((((r * 4) + (tr_col >> 3)) ^ vswz_key(tr_key)) * 16) + (tr_col & 7) * 2;
+    for (int d = 0; d < DB; ++d)
+        v_off[d] = tr_key * (T::VGR * 16) + vswz<T::VGR>(tr_key, d * 4 + (tr_col >> 3)) * 16 + (tr_col & 7) * 2;
 
     float m_run[2] = {-INFINITY, -INFINITY};  // max used by exp2 (log2 units), refreshed lazily
     float l_part[2] = {0.f, 0.f};            // this lane's share of the softmax denominator
@@ -521,14 +546,15 @@ void attn_fwd_kernel(AttnArgs a) {
             for (int i = 0; i < 16; ++i) o[d][nb][i] = 0.f;
 
     auto load_kfrag = [&](const char* kt_buf, int ks, int mb) -> bf16x8 {
-        const u32x4 raw = *(const u32x4*)(kt_buf + mb * 32 * T::KGR * 16 + (ks >> 2) * 128 + k_off[ks & 3]);
+        const u32x4 raw = *(const u32x4*)(kt_buf + mb * 32 * T::KGR * 16 + (ks / K_OFFS) * (K_OFFS * 32) +
+                                          k_off[ks % K_OFFS]);
         return __builtin_bit_cast(bf16x8, raw);
     };
     auto load_vfrag = [&](const char* vt, int mb, int hh, int d) -> bf16x8 {
         bf16x8 af;
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-            const char* addr = vt + (mb * 32 + hh * 16 + half * 8) * T::VGR * 16 + (d >> 1) * 128 + v_off[d & 1];
+            const char* addr = vt + (mb * 32 + hh * 16 + half * 8) * T::VGR * 16 + v_off[d];
             const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(addr));
             const bf16x4 rb = __builtin_bit_cast(bf16x4, r);
 #pragma unroll
@@ -564,24 +590,34 @@ void attn_fwd_kernel(AttnArgs a) {
         wait_vmcnt<0>();
         lds_barrier();  // K(t+1), V(t) are in LDS; every wave is done with K(t) and V(t-1)
         // the next tiles' copies (K(t+2) into the K buffer just freed, V(t+1)
-        // into the V buffer just freed) are spread over the first slots
-        const bool do_k = t + 2 < ntiles;
-        const bool do_v = has_next && t + 1 < ntiles;
-        const i32x4 rk = k_rsrc(do_k ? kt + 2 * BN : kb);
-        const i32x4 rv = v_rsrc(do_v ? kt + BN : kb);
+        // into the V buffer just freed) are spread over the first slots. Past
+        // the last tile the resources are empty: the copies then only write
+        // zeros into buffers that no later step reads, and the step needs no
+        // branch around them.
+        const i32x4 rk = k_rsrc(kt + 2 * BN);
+        const i32x4 rv = v_rsrc(kt + BN);
 
         // causal / range mask on the tiles that cross a row's last visible key:
         // key kt + c (c = mb*32 + (i>>2)*8 + lg*4 + (i&3)) is hidden when
         // c > qlim - kt, with qlim = min(row position, ke - 1) - lg*4
         if ((kt + BN - 1 > wave_first) || (kt + BN > ke)) {
+            const float ninf = -INFINITY;
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb) {
                 const int lim = qlim[nb] - kt;
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        if (mb * 32 + (i >> 2) * 8 + (i & 3) > lim) s_cur[mb][nb][i] = -INFINITY;
+                    for (int i = 0; i < 16; ++i) {
+                        // compare and select through VCC, one element at a time (no
+                        // batch of 64-bit lane masks in scalar registers)
+                        float x = s_cur[mb][nb][i];
+                        asm("v_cmp_gt_i32 vcc, %2, %1\n\tv_cndmask_b32 %0, %0, %3, vcc"
+                            : "+v"(x)
+                            : "v"(lim), "i"(mb * 32 + (i >> 2) * 8 + (i & 3)), "v"(ninf)
+                            : "vcc");
+                        s_cur[mb][nb][i] = x;
+                    }
             }
         }
 
@@ -664,9 +700,9 @@ void attn_fwd_kernel(AttnArgs a) {
                     if constexpr (s % LSTRIDE == 0 && s / LSTRIDE < NL) {
                         constexpr int j = s / LSTRIDE;
                         if constexpr (j < T::V_LOADS) {
-                            if (do_v) load_v(rv, vbuf0 + (1 - par) * T::V_BYTES, j);
+                            load_v(rv, std::integral_constant<int, 1 - par>(), std::integral_constant<int, j>());
                         } else {
-                            if (do_k) load_k(rk, kbuf0 + par * T::K_BYTES, j - T::V_LOADS);
+                            load_k(rk, std::integral_constant<int, par>(), std::integral_constant<int, j - T::V_LOADS>());
                         }
                     }
                 }
@@ -725,18 +761,29 @@ void attn_fwd_kernel(AttnArgs a) {
         }
         if (t < ntiles) step(P0(), LAST(), t, s_a, s_b);
         mfma_drain();
+        // a pair's second step may still be copying (zeros) into LDS: no copy
+        // may outlive the workgroup's LDS allocation
+        wait_vmcnt<0>();
     }
 
     // ---- epilogue: normalise and store ----
+    // The arguments only the epilogue needs are read again from the kernel
+    // argument segment (the empty asm hides that they were read before), so
+    // they do not occupy scalar registers across the key loop.
+    const AttnArgs* ka = (const AttnArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(ka));
+    const WorkItem it2 = ka->items[item_id];
+    const int row0 = __builtin_amdgcn_readfirstlane(it2.row0);
+    const int split = __builtin_amdgcn_readfirstlane(it2.split);
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
         const float l_tot = lane_swap32_add(l_part[nb]);
         const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
         const float lse_val = l_tot > 0.f ? (m_run[nb] + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
         if (!qvalid[nb]) continue;
-        const int row = it.row0 + wave * 64 + nb * 32 + lr;
+        const int row = row0 + wave * 64 + nb * 32 + lr;
         if constexpr (SPLIT) {
-            float* po = (float*)a.out + (((int64_t)it.split * a.tokens + row) * a.num_heads + h) * DV;
+            float* po = (float*)ka->out + (((int64_t)split * ka->tokens + row) * ka->num_heads + h) * DV;
 #pragma unroll
             for (int d = 0; d < DB; ++d)
 #pragma unroll
@@ -745,9 +792,9 @@ void attn_fwd_kernel(AttnArgs a) {
                                 o[d][nb][c * 4 + 2] * inv_l, o[d][nb][c * 4 + 3] * inv_l};
                     *(float4*)(po + d * 32 + c * 8 + lg * 4) = w;
                 }
-            if (lg == 0) a.lse[((int64_t)it.split * a.num_heads + h) * a.tokens + row] = lse_val;
+            if (lg == 0) ka->lse[((int64_t)split * ka->num_heads + h) * ka->tokens + row] = lse_val;
         } else {
-            u16* op = (u16*)a.out + (int64_t)row * a.o_st + (int64_t)h * a.o_sh;
+            u16* op = (u16*)ka->out + (int64_t)row * ka->o_st + (int64_t)h * ka->o_sh;
 #pragma unroll
             for (int d = 0; d < DB; ++d)
 #pragma unroll
@@ -757,7 +804,7 @@ void attn_fwd_kernel(AttnArgs a) {
                     for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][nb][c * 4 + j] * inv_l);
                     *(bf16x4*)(op + d * 32 + c * 8 + lg * 4) = w;
                 }
-            if (lg == 0 && a.lse) a.lse[(int64_t)h * a.lse_sh + row] = lse_val;
+            if (lg == 0 && ka->lse) ka->lse[(int64_t)h * ka->lse_sh + row] = lse_val;
         }
     }
 }
