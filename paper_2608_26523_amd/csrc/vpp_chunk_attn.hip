@@ -36,9 +36,11 @@
 
 namespace {
 
-constexpr int BM = 256;        // query rows per workgroup tile (4 waves x 64 rows)
 constexpr int BN = 64;         // keys per inner step
 constexpr int NWAVES = 4;
+// query rows per workgroup tile: 4 waves x NB blocks of 32 rows
+constexpr int block_rows(int nb) { return 32 * nb * NWAVES; }
+constexpr int BM_MAX = block_rows(2);
 constexpr int NTHREADS = 64 * NWAVES;
 constexpr int MAX_SPLITS = 16;
 constexpr int STAGING_SLOTS = 4;
@@ -185,7 +187,7 @@ __device__ __forceinline__ void work_coords(const AttnArgs& a, int& item, int& h
     item = (int)(L % a.num_items);
 }
 
-template <int DQK, int DV>
+template <int DQK, int DV, int NB>
 struct Tiles {
     static constexpr int KS = DQK / 16;          // MFMA k-steps of S^T = K Q^T
     static constexpr int DB = DV / 32;           // 32-row blocks of O^T
@@ -196,20 +198,21 @@ struct Tiles {
     static constexpr int BYTES = 2 * K_BYTES + 2 * V_BYTES;  // double-buffered K and V
     static constexpr int K_LOADS = BN * KGR / 64 / NWAVES;   // 16-byte loads per lane per tile
     static constexpr int V_LOADS = BN * VGR / 64 / NWAVES;
-    static constexpr int NQK = 4 * KS;           // MFMAs of one S^T tile (2 key blocks x 2 query blocks)
-    static constexpr int NPV = 8 * DB;           // MFMAs of one O^T update (4 key groups x 2 query blocks)
+    static constexpr int NQK = 2 * KS * NB;      // MFMAs of one S^T tile (2 key blocks x NB query blocks)
+    static constexpr int NPV = 4 * DB * NB;      // MFMAs of one O^T update (4 key groups x NB query blocks)
     static_assert(KGR % 8 == 0 && VGR % 8 == 0, "swizzle needs 8 granules per row");
     static_assert(BN * KGR % (64 * NWAVES) == 0 && BN * VGR % (64 * NWAVES) == 0, "whole wave loads");
 };
 
 // S^T MFMA i of a tile: key block mb = 1 first, so that the block-0
 // accumulators of the next tile are written only after the softmax has
-// consumed this tile's block 0 and their registers can be reused.
-template <int KS>
+// consumed this tile's block 0 and their registers can be reused. Within a
+// key block the k-steps run in order, each K fragment feeding NB MFMAs.
+template <int KS, int NB>
 struct QkCoords {
-    static constexpr int mb(int i) { return 1 - i / (2 * KS); }
-    static constexpr int ks(int i) { return (i % (2 * KS)) >> 1; }
-    static constexpr int nb(int i) { return i & 1; }
+    static constexpr int mb(int i) { return 1 - i / (KS * NB); }
+    static constexpr int ks(int i) { return (i % (KS * NB)) / NB; }
+    static constexpr int nb(int i) { return i % NB; }
 };
 
 // ---------------------------------------------------------------------------
@@ -218,65 +221,73 @@ struct QkCoords {
 // One wave (one SIMD) runs, per tile, NQK MFMAs of the next tile's S^T, NPV
 // MFMAs of this tile's O^T update and the softmax of this tile in fp32 VALU
 // code. A wave issues in order; VALU work issued right after an MFMA runs
-// while the matrix core is busy (about 5 VALU instructions fit under one
-// 32x32x16 MFMA), so the softmax is cut into small atoms spread evenly over
-// the MFMA slots:
-//   atoms 0..7     4 v_max3 steps of the row max (query block nb = a >> 2)
-//   atoms 8, 9     finish the row max of block 0 / 1: lane exchange, lazy
-//                  rescale decision, new reference max
-//   atoms 10..73   one score each: exp2, row sum, bf16 packing; element
-//                  e = a - 10 belongs to unit u = e >> 3, which holds the 8 P
-//                  values one O^T MFMA group consumes:
-//                  (key block mb, 16-key group hh, query block nb) = (u>>2, (u>>1)&1, u&1)
-// O^T MFMA p works on key group g = p / (2*DB) (units 2g, 2g+1), value block
-// d = (p / 2) % DB and query block nb = p % 2, so each V^T fragment feeds two
-// MFMAs in a row; it is placed only after both units' atoms. All atoms finish
-// before the last group's MFMAs start.
+// while the matrix core is busy, so the softmax is cut into small atoms
+// spread over the MFMA slots. With NB query blocks of 32 rows per wave:
+//   atoms 0 .. 4NB-1      4 v_max3 steps of the row max per query block
+//                         (block nb = a / 4)
+//   atoms 4NB .. 5NB-1    finish the row max of block nb: lane exchange, lazy
+//                         rescale decision, new reference max
+//   atoms 5NB .. 37NB-1   one score each: exp2, row sum, bf16 packing;
+//                         element e belongs to unit u = e / 8, which holds the
+//                         8 P values one O^T MFMA consumes: query block
+//                         nb = u % NB, 16-key group hh = (u / NB) % 2, key
+//                         block mb = u / (2 NB)
+// O^T MFMA p works on key group g = p / (NB*DB) (units g*NB .. g*NB+NB-1),
+// value block d = (p / NB) % DB and query block nb = p % NB, so each V^T
+// fragment feeds NB MFMAs in a row; it is placed only after its group's atoms.
+// All atoms finish before the last group's MFMAs start.
 // ---------------------------------------------------------------------------
-constexpr int N_ATOMS = 74;
-constexpr int ATOM_MAXF = 8;   // first finishing atom
-constexpr int ATOM_EXP = 10;   // first exp atom
-constexpr int atom_weight(int k) { return k < ATOM_MAXF ? 24 : (k < ATOM_EXP ? 70 : 23); }  // VALU cycles
-constexpr int unit_last_atom(int u) { return ATOM_EXP + 8 * u + 7; }
+template <int NB>
+struct Atoms {
+    static constexpr int N = 37 * NB;
+    static constexpr int MAXF = 4 * NB;  // first finishing atom
+    static constexpr int EXP = 5 * NB;   // first exp atom
+    static constexpr int weight(int k) { return k < MAXF ? 24 : (k < EXP ? 70 : 23); }  // VALU cycles
+    static constexpr int unit_last(int u) { return EXP + 8 * u + 7; }
+};
 
-template <int NQK, int NPV, int DB>
+template <int NQK, int NPV, int DB, int NB>
 struct Schedule {
+    typedef Atoms<NB> A;
     // the last tile has no next S^T to overlap with: it opens with one
-    // VALU-only slot for the row max, then hides each unit's atoms under the
-    // previous unit's MFMAs
+    // VALU-only slot for the row max, then hides each key group's atoms under
+    // the previous group's MFMAs
     static constexpr int NS = NQK + NPV + (NQK == 0 ? 1 : 0);
+    static constexpr int GROUP_PV = NB * DB;  // O^T MFMAs per key group
     int kind[NS] = {};      // 0: S^T MFMA, 1: O^T MFMA, 2: no MFMA
-    int index[NS] = {};     // S^T: see QkCoords; O^T: see PvCoords
+    int index[NS] = {};     // S^T: see QkCoords; O^T: see above
     int atoms_end[NS] = {}; // atoms issued after slot s: [atoms_end[s-1], atoms_end[s])
     int rescale_before = 0; // slot before which the (rare) O rescale check runs
     constexpr Schedule() {
-        int done_at[N_ATOMS] = {};
+        int done_at[A::N] = {};
         if constexpr (NQK == 0) {
             kind[0] = 2;
-            for (int k = 0; k < ATOM_EXP + 8; ++k) done_at[k] = 0;
+            for (int k = 0; k < A::EXP + 8 * NB; ++k) done_at[k] = 0;
             for (int p = 0; p < NPV; ++p) {
                 kind[1 + p] = 1;
                 index[1 + p] = p;
             }
-            for (int g = 1; g < 4; ++g)  // key group g (units 2g, 2g+1) under group g-1's MFMAs
-                for (int j = 0; j < 16; ++j) done_at[ATOM_EXP + 16 * g + j] = 1 + (g - 1) * 2 * DB + (j * 2 * DB) / 16;
+            for (int g = 1; g < 4; ++g)  // key group g under group g-1's MFMAs
+                for (int j = 0; j < 8 * NB; ++j)
+                    done_at[A::EXP + 8 * NB * g + j] = 1 + (g - 1) * GROUP_PV + (j * GROUP_PV) / (8 * NB);
         } else {
             // slot by which each atom is done: spread by weight over the slots
-            // before the last unit's MFMAs
+            // before the last group's MFMAs
             int total = 0;
-            for (int k = 0; k < N_ATOMS; ++k) total += atom_weight(k);
-            const int span = NS - 2 * DB;
+            for (int k = 0; k < A::N; ++k) total += A::weight(k);
+            const int span = NS - GROUP_PV;
             int acc = 0;
-            for (int k = 0; k < N_ATOMS; ++k) {
-                acc += atom_weight(k);
+            for (int k = 0; k < A::N; ++k) {
+                acc += A::weight(k);
                 int s = (acc * span + total - 1) / total - 1;
                 done_at[k] = s < 0 ? 0 : s;
             }
             // MFMA order: an O^T MFMA as soon as its key group's atoms are done, else an S^T MFMA
             int q = 0, p = 0;
             for (int s = 0; s < NS; ++s) {
-                const int grp = p / (2 * DB);
-                const bool pv_ready = p < NPV && done_at[ATOM_EXP - 1] < s && done_at[unit_last_atom(2 * grp + 1)] < s;
+                const int grp = p / GROUP_PV;
+                const bool pv_ready = p < NPV && done_at[A::EXP - 1] < s &&
+                                      done_at[A::unit_last(grp * NB + NB - 1)] < s;
                 if (pv_ready || q >= NQK) {
                     kind[s] = 1;
                     index[s] = p++;
@@ -288,7 +299,7 @@ struct Schedule {
         }
         for (int s = 0; s < NS; ++s) {
             int n = 0;
-            for (int k = 0; k < N_ATOMS; ++k) n += done_at[k] <= s;
+            for (int k = 0; k < A::N; ++k) n += done_at[k] <= s;
             atoms_end[s] = n;
         }
         rescale_before = NS;
@@ -300,11 +311,11 @@ struct Schedule {
         for (int s = 0; s < NS; ++s) {
             if (s > 0 && atoms_end[s] < atoms_end[s - 1]) return false;
             if (kind[s] != 1) continue;
-            const int grp = index[s] / (2 * DB);
+            const int grp = index[s] / GROUP_PV;
             const int before = s == 0 ? 0 : atoms_end[s - 1];
-            if (before < unit_last_atom(2 * grp + 1) + 1) return false;
+            if (before < A::unit_last(grp * NB + NB - 1) + 1) return false;
         }
-        return atoms_end[NS - 1] == N_ATOMS;
+        return atoms_end[NS - 1] == A::N;
     }
 };
 
@@ -411,14 +422,19 @@ __device__ __forceinline__ void static_range(F&& f) {
     static_range_impl<A0>(f, std::make_integer_sequence<int, A1 - A0>());
 }
 
-template <int DQK, int DV, bool SPLIT>
-__global__ __attribute__((amdgpu_flat_work_group_size(NTHREADS, NTHREADS), amdgpu_waves_per_eu(1, 1)))
+// NB = 2: 64 query rows per wave, one workgroup (4 waves) per CU. NB = 1: 32
+// rows per wave and half the registers, so two workgroups share a CU and each
+// SIMD interleaves two waves' instruction streams.
+template <int DQK, int DV, int NB, bool SPLIT>
+__global__ __attribute__((amdgpu_flat_work_group_size(NTHREADS, NTHREADS), amdgpu_waves_per_eu(3 - NB, 3 - NB)))
 void attn_fwd_kernel(AttnArgs a) {
-    typedef Tiles<DQK, DV> T;
+    typedef Tiles<DQK, DV, NB> T;
+    typedef Atoms<NB> A;
     constexpr int KS = T::KS;
     constexpr int DB = T::DB;
-    typedef Schedule<T::NQK, T::NPV, DB> SchedFull;
-    typedef Schedule<0, T::NPV, DB> SchedLast;
+    constexpr int WROWS = 32 * NB;  // query rows per wave
+    typedef Schedule<T::NQK, T::NPV, DB, NB> SchedFull;
+    typedef Schedule<0, T::NPV, DB, NB> SchedLast;
     static_assert(SchedFull().valid() && SchedLast().valid(), "tile schedule breaks a dependency");
 
     __shared__ __attribute__((aligned(1024))) char smem[T::BYTES];
@@ -450,22 +466,22 @@ void attn_fwd_kernel(AttnArgs a) {
     const u16* vbase = a.v + it.kv_base * a.v_st + (int64_t)hk * a.v_sh;
     const int ntiles = (ke - kb + BN - 1) / BN;
 
-    // This lane's two query rows (one per 32-column block of S^T), as B
+    // This lane's NB query rows (one per 32-column block of S^T), as B
     // operands in AGPRs. Rows past the tile re-read its last row (their results
     // are never stored), so every load stays inside q.
-    bf16x8 qf[2][KS];
-    int qlim[2];   // last key position the row may see, minus lg*4 (see masking)
-    bool qvalid[2];
+    bf16x8 qf[NB][KS];
+    int qlim[NB];   // last key position the row may see, minus lg*4 (see masking)
+    bool qvalid[NB];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        const int rloc = wave * 64 + nb * 32 + lr;
+    for (int nb = 0; nb < NB; ++nb) {
+        const int rloc = wave * WROWS + nb * 32 + lr;
         qvalid[nb] = rloc < it.nrows;
         qlim[nb] = min(it.pos0 + rloc, ke - 1) - lg * 4;
         const u16* qp = a.q + (int64_t)(it.row0 + min(rloc, it.nrows - 1)) * a.q_st + (int64_t)h * a.q_sh + lg * 8;
         load_q_agpr<KS>(qf[nb], qp);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    const int wave_first = it.pos0 + wave * 64;
+    const int wave_first = it.pos0 + wave * WROWS;
 
     // Global->LDS copy of one tile through a buffer resource whose base is the
     // tile's first key row and whose size ends at the last key of the range:
@@ -535,13 +551,18 @@ void attn_fwd_kernel(AttnArgs a) {
     for (int d = 0; d < DB; ++d)
         v_off[d] = tr_key * (T::VGR * 16) + vswz<T::VGR>(tr_key, d * 4 + (tr_col >> 3)) * 16 + (tr_col & 7) * 2;
 
-    float m_run[2] = {-INFINITY, -INFINITY};  // max used by exp2 (log2 units), refreshed lazily
-    float l_part[2] = {0.f, 0.f};            // this lane's share of the softmax denominator
-    f32x16 o[DB][2];
+    float m_run[NB];   // max used by exp2 (log2 units), refreshed lazily
+    float l_part[NB];  // this lane's share of the softmax denominator
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        m_run[nb] = -INFINITY;
+        l_part[nb] = 0.f;
+    }
+    f32x16 o[DB][NB];
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
             for (int i = 0; i < 16; ++i) o[d][nb][i] = 0.f;
 
@@ -564,14 +585,14 @@ void attn_fwd_kernel(AttnArgs a) {
     };
 
     // S^T = K Q^T for a whole tile (prologue only: no softmax to overlap with)
-    auto qk_all = [&](const char* kt_buf, f32x16 (&s)[2][2]) {
+    auto qk_all = [&](const char* kt_buf, f32x16 (&s)[2][NB]) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) {
                 const bf16x8 af = load_kfrag(kt_buf, ks, mb);
 #pragma unroll
-                for (int nb = 0; nb < 2; ++nb) {
+                for (int nb = 0; nb < NB; ++nb) {
                     const bf16x8 bq = qf[nb][ks];
                     if (ks == 0) MFMA_32x32x16_INIT(s[mb][nb], af, bq);
                     else MFMA_32x32x16_ACC(s[mb][nb], af, bq);
@@ -581,7 +602,7 @@ void attn_fwd_kernel(AttnArgs a) {
 
     // One key tile: mask S(t) if needed, then the scheduled mix of S(t+1)
     // MFMAs, the softmax of S(t) and the O^T += V^T P^T MFMAs of tile t.
-    auto step = [&](auto P, auto HAS_NEXT, int t, f32x16 (&s_cur)[2][2], f32x16 (&s_nxt)[2][2]) {
+    auto step = [&](auto P, auto HAS_NEXT, int t, f32x16 (&s_cur)[2][NB], f32x16 (&s_nxt)[2][NB]) {
         constexpr int par = decltype(P)::value;
         constexpr bool has_next = decltype(HAS_NEXT)::value;
         const char* kt_nxt = kbuf0 + (1 - par) * T::K_BYTES;
@@ -603,7 +624,7 @@ void attn_fwd_kernel(AttnArgs a) {
         if ((kt + BN - 1 > wave_first) || (kt + BN > ke)) {
             const float ninf = -INFINITY;
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < NB; ++nb) {
                 const int lim = qlim[nb] - kt;
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
@@ -621,18 +642,24 @@ void attn_fwd_kernel(AttnArgs a) {
             }
         }
 
-        float alpha[2] = {1.f, 1.f}, m_use[2] = {0.f, 0.f};
-        bool refresh[2] = {false, false};
-        float mx[2] = {-INFINITY, -INFINITY};
-        float lsum[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
+        float alpha[NB], m_use[NB], mx[NB], lsum[NB][2];
+        bool refresh[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            alpha[nb] = 1.f;
+            m_use[nb] = 0.f;
+            mx[nb] = -INFINITY;
+            lsum[nb][0] = lsum[nb][1] = 0.f;
+            refresh[nb] = false;
+        }
         float pprev = 0.f;
-        bf16x8 pb[2][2][2];          // [nb][mb][hh]
+        bf16x8 pb[NB][2][2];         // [nb][mb][hh]
         bf16x8 kf[4];                // K fragments in issue order, three in flight
         bf16x8 vf[3];                // V^T fragments in issue order, two in flight
 
         auto atom = [&](auto K) {
             constexpr int k = decltype(K)::value;
-            if constexpr (k < ATOM_MAXF) {
+            if constexpr (k < A::MAXF) {
                 // 4 max3 steps over 8 of the 32 scores of query block nb
                 constexpr int nb = k >> 2, q = k & 3;
 #pragma unroll
@@ -640,8 +667,8 @@ void attn_fwd_kernel(AttnArgs a) {
                     const int v = q * 8 + j;  // score index in [mb*16 + i]
                     mx[nb] = max3f(mx[nb], s_cur[v >> 4][nb][v & 15], s_cur[(v + 1) >> 4][nb][(v + 1) & 15]);
                 }
-            } else if constexpr (k < ATOM_EXP) {
-                constexpr int nb = k - ATOM_MAXF;
+            } else if constexpr (k < A::EXP) {
+                constexpr int nb = k - A::MAXF;
                 const float m = lane_swap32_max(mx[nb]) * a.scale_log2;
                 refresh[nb] = __builtin_amdgcn_ballot_w64(m > m_run[nb] + LAZY_TAU) != 0;
                 const float m_new = refresh[nb] ? fmaxf(m_run[nb], m) : m_run[nb];
@@ -651,9 +678,9 @@ void attn_fwd_kernel(AttnArgs a) {
                 m_use[nb] = (m_new == -INFINITY) ? 0.f : m_new;
                 l_part[nb] *= alpha[nb];
             } else {
-                constexpr int e = k - ATOM_EXP;
+                constexpr int e = k - A::EXP;
                 constexpr int u = e >> 3, j = e & 7;
-                constexpr int mb = u >> 2, hh = (u >> 1) & 1, nb = u & 1;
+                constexpr int mb = u / (2 * NB), hh = (u / NB) & 1, nb = u % NB;
                 const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mb][nb][hh * 8 + j], a.scale_log2, -m_use[nb]));
                 lsum[nb][j & 1] += pv;
                 if constexpr ((j & 1) == 0) {
@@ -669,25 +696,28 @@ void attn_fwd_kernel(AttnArgs a) {
             typedef typename decltype(tag)::type Sch;
             constexpr Sch sch{};
             constexpr int NS = Sch::NS;
-            typedef QkCoords<KS> C;
+            typedef QkCoords<KS, NB> C;
             // fragments needed first: two V^T fragments, and three K fragments of the next tile
             vf[0] = load_vfrag(vt_cur, 0, 0, 0);
             vf[1] = load_vfrag(vt_cur, 0, 0, 1 % DB);
             if constexpr (has_next) {
                 kf[0] = load_kfrag(kt_nxt, C::ks(0), C::mb(0));
-                kf[1] = load_kfrag(kt_nxt, C::ks(2), C::mb(2));
-                kf[2] = load_kfrag(kt_nxt, C::ks(4), C::mb(4));
+                kf[1] = load_kfrag(kt_nxt, C::ks(NB), C::mb(NB));
+                kf[2] = load_kfrag(kt_nxt, C::ks(2 * NB), C::mb(2 * NB));
             }
             static_for<NS>([&](auto SL) {
                 constexpr int s = SL;
                 constexpr int kind = sch.kind[s];
                 constexpr int idx = sch.index[s];
                 if constexpr (s == sch.rescale_before) {
-                    if (refresh[0] || refresh[1]) {
+                    bool any = false;
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb) any = any || refresh[nb];
+                    if (any) {
                         // rare: rescale the AGPR accumulators 16 at a time, so the
                         // branch needs only a few temporary VGPRs
                         mfma_drain();
-                        static_for<2 * DB>([&](auto J) {
+                        static_for<NB * DB>([&](auto J) {
                             constexpr int nb = J / DB, d = J % DB;
                             scale_agpr_tile(o[d][nb], alpha[nb]);
                             __builtin_amdgcn_sched_barrier(0);
@@ -710,18 +740,18 @@ void attn_fwd_kernel(AttnArgs a) {
                     // VALU-only slot
                 } else if constexpr (kind == 0) {
                     constexpr int ks = C::ks(idx), mb = C::mb(idx), nb = C::nb(idx);
-                    constexpr int frag = idx >> 1;  // (mb, ks) in issue order
+                    constexpr int frag = idx / NB;  // (mb, ks) in issue order
                     // prefetch three fragments ahead with this fragment's first MFMA
                     if constexpr (nb == 0 && frag + 3 < 2 * KS)
-                        kf[(frag + 3) % 4] = load_kfrag(kt_nxt, C::ks(2 * (frag + 3)), C::mb(2 * (frag + 3)));
+                        kf[(frag + 3) % 4] = load_kfrag(kt_nxt, C::ks(NB * (frag + 3)), C::mb(NB * (frag + 3)));
                     const bf16x8 af = kf[frag % 4];
                     const bf16x8 bq = qf[nb][ks];
                     if constexpr (ks == 0) MFMA_32x32x16_INIT(s_nxt[mb][nb], af, bq);
                     else MFMA_32x32x16_ACC(s_nxt[mb][nb], af, bq);
                 } else {
-                    constexpr int grp = idx / (2 * DB), d = (idx >> 1) % DB, nb = idx & 1;
+                    constexpr int grp = idx / (NB * DB), d = (idx / NB) % DB, nb = idx % NB;
                     constexpr int mb = grp >> 1, hh = grp & 1;
-                    constexpr int frag = idx >> 1;  // (grp, d) in issue order
+                    constexpr int frag = idx / NB;  // (grp, d) in issue order
                     // prefetch two fragments ahead with this fragment's first MFMA
                     if constexpr (nb == 0 && frag + 2 < 4 * DB) {
                         constexpr int f2 = frag + 2;
@@ -738,7 +768,7 @@ void attn_fwd_kernel(AttnArgs a) {
         if constexpr (has_next) run(std::type_identity<SchedFull>());
         else run(std::type_identity<SchedLast>());
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) l_part[nb] += lsum[nb][0] + lsum[nb][1];
+        for (int nb = 0; nb < NB; ++nb) l_part[nb] += lsum[nb][0] + lsum[nb][1];
     };
 
     if (ntiles > 0) {
@@ -746,7 +776,7 @@ void attn_fwd_kernel(AttnArgs a) {
         typedef std::integral_constant<int, 1> P1;
         typedef std::integral_constant<bool, true> NX;
         typedef std::integral_constant<bool, false> LAST;
-        f32x16 s_a[2][2], s_b[2][2];
+        f32x16 s_a[2][NB], s_b[2][NB];
         wait_vmcnt<0>();
         lds_barrier();
         qk_all(kbuf0, s_a);
@@ -776,12 +806,12 @@ void attn_fwd_kernel(AttnArgs a) {
     const int row0 = __builtin_amdgcn_readfirstlane(it2.row0);
     const int split = __builtin_amdgcn_readfirstlane(it2.split);
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
         const float l_tot = lane_swap32_add(l_part[nb]);
         const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
         const float lse_val = l_tot > 0.f ? (m_run[nb] + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
         if (!qvalid[nb]) continue;
-        const int row = row0 + wave * 64 + nb * 32 + lr;
+        const int row = row0 + wave * WROWS + nb * 32 + lr;
         if constexpr (SPLIT) {
             float* po = (float*)ka->out + (((int64_t)split * ka->tokens + row) * ka->num_heads + h) * DV;
 #pragma unroll
@@ -867,6 +897,7 @@ struct vpp_chunk_attn_plan_s {
     std::vector<WorkItem> items;
     int32_t num_tiles = 0;
     int32_t num_splits = 1;
+    int32_t nb = 2;  // 32-row query blocks per wave of the kernel variant the plan was made for
     int32_t tokens = 0;
     double pairs = 0.0;
     size_t items_bytes = 0;
@@ -886,11 +917,20 @@ bool supported_dims(int dqk, int dv) {
     return (dqk == 64 && dv == 64) || (dqk == 128 && dv == 128) || (dqk == 192 && dv == 128);
 }
 
+// Kernel variant for a configuration: query blocks of 32 rows per wave
+// (VPP_NB overrides, for tuning).
+int choose_nb(const vpp_chunk_attn_config_t& c) {
+    const char* e = getenv("VPP_NB");
+    if (e && (atoi(e) == 1 || atoi(e) == 2)) return atoi(e);
+    (void)c;
+    return 2;
+}
+
 vpp_status_t check_config(const vpp_chunk_attn_config_t& c) {
     if (c.num_q_heads <= 0 || c.num_kv_heads <= 0 || c.num_q_heads % c.num_kv_heads != 0)
         return VPP_ERR_INVALID_ARG;
     if (c.max_chunk_tokens <= 0 || c.max_segments <= 0 || c.max_kv_len <= 0) return VPP_ERR_INVALID_ARG;
-    if (c.max_kv_len > (int64_t)INT32_MAX - BM) return VPP_ERR_INVALID_ARG;
+    if (c.max_kv_len > (int64_t)INT32_MAX - BM_MAX) return VPP_ERR_INVALID_ARG;
     if (!(c.softmax_scale >= 0.f) || !isfinite(c.softmax_scale)) return VPP_ERR_INVALID_ARG;
     if (c.num_splits == 0 || c.num_splits < -1 || c.num_splits > MAX_SPLITS) return VPP_ERR_INVALID_ARG;
     if (c.causal != 1) return VPP_ERR_UNSUPPORTED;
@@ -942,6 +982,8 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
     if (cu_q[num_segments] > c.max_chunk_tokens) return VPP_ERR_INVALID_ARG;
 
     // query tiles of every segment, with their whole key range [0, last position + 1)
+    const int nb = p ? p->nb : choose_nb(c);
+    const int BM = block_rows(nb);
     std::vector<WorkItem> tiles;
     double pairs = 0.0, key_tiles = 0.0;
     try {
@@ -996,6 +1038,7 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
         p = new (std::nothrow) vpp_chunk_attn_plan_s();
         if (!p) return VPP_ERR_NOMEM;
         p->cfg = c;
+        p->nb = nb;
         *inout_plan = p;
     }
     p->scale = c.softmax_scale > 0.f ? c.softmax_scale : (float)(1.0 / sqrt((double)c.head_dim_qk));
@@ -1020,7 +1063,7 @@ extern "C" vpp_status_t vpp_chunk_attn_plan_info(vpp_chunk_attn_plan_t p, vpp_ch
     info->num_tiles = p->num_tiles;
     info->num_splits = p->num_splits;
     info->num_work_items = (int32_t)p->items.size();
-    info->block_m = BM;
+    info->block_m = block_rows(p->nb);
     info->block_n = BN;
     info->num_tokens = p->tokens;
     info->workspace_bytes = (int64_t)p->ws_bytes;
@@ -1069,21 +1112,21 @@ namespace {
 bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 bool stride_ok(int64_t s) { return s > 0 && (s % 8) == 0; }
 
-template <int DQK, int DV>
+template <int DQK, int DV, int NB>
 hipError_t launch(const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
     const int64_t total = (int64_t)a.num_items * a.num_heads;
     if (total <= 0) return hipSuccess;
     if (total > (int64_t)INT32_MAX) return hipErrorInvalidValue;
     dim3 grid((unsigned)total), block(NTHREADS);
     if (split) {
-        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, true>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, true>), grid, block, 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int64_t threads = (int64_t)ca.tokens * ca.num_heads * (DV / 4);
         dim3 cg((unsigned)((threads + 255) / 256));
         hipLaunchKernelGGL((combine_kernel<DV>), cg, dim3(256), 0, stream, ca);
     } else {
-        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, false>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, false>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
 }
@@ -1179,8 +1222,14 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
         ca.splits = p->num_splits;
     }
     hipError_t e;
-    if (c.head_dim_qk == 64) e = launch<64, 64>(a, split, ca, stream);
-    else if (c.head_dim_qk == 128) e = launch<128, 128>(a, split, ca, stream);
-    else e = launch<192, 128>(a, split, ca, stream);
+    if (p->nb == 1) {
+        if (c.head_dim_qk == 64) e = launch<64, 64, 1>(a, split, ca, stream);
+        else if (c.head_dim_qk == 128) e = launch<128, 128, 1>(a, split, ca, stream);
+        else e = launch<192, 128, 1>(a, split, ca, stream);
+    } else {
+        if (c.head_dim_qk == 64) e = launch<64, 64, 2>(a, split, ca, stream);
+        else if (c.head_dim_qk == 128) e = launch<128, 128, 2>(a, split, ca, stream);
+        else e = launch<192, 128, 2>(a, split, ca, stream);
+    }
     return e == hipSuccess ? VPP_OK : VPP_ERR_HIP;
 }
