@@ -600,6 +600,13 @@ void attn_fwd_kernel(AttnArgs a) {
             }
     };
 
+    // Running sources of the copies a step issues (K(t+2) and V(t+1)): scalar
+    // pointer and remaining row count, advanced by one tile per step.
+    const int k_row_bytes = (int)a.k_st * 2, v_row_bytes = (int)a.v_st * 2;
+    uint64_t k_next = (uint64_t)(uintptr_t)(kbase + (int64_t)(kb + 2 * BN) * a.k_st);
+    uint64_t v_next = (uint64_t)(uintptr_t)(vbase + (int64_t)(kb + BN) * a.v_st);
+    int k_rows = ke - kb - 2 * BN, v_rows = ke - kb - BN;
+
     // One key tile: mask S(t) if needed, then the scheduled mix of S(t+1)
     // MFMAs, the softmax of S(t) and the O^T += V^T P^T MFMAs of tile t.
     auto step = [&](auto P, auto HAS_NEXT, int t, f32x16 (&s_cur)[2][NB], f32x16 (&s_nxt)[2][NB]) {
@@ -615,8 +622,14 @@ void attn_fwd_kernel(AttnArgs a) {
         // the last tile the resources are empty: the copies then only write
         // zeros into buffers that no later step reads, and the step needs no
         // branch around them.
-        const i32x4 rk = k_rsrc(kt + 2 * BN);
-        const i32x4 rv = v_rsrc(kt + BN);
+        const int k_bytes = k_rows >= BN ? BN * k_row_bytes : (k_rows > 0 ? k_rows * k_row_bytes : 0);
+        const int v_bytes = v_rows >= BN ? BN * v_row_bytes : (v_rows > 0 ? v_rows * v_row_bytes : 0);
+        const i32x4 rk = make_rsrc((const void*)k_next, k_bytes);
+        const i32x4 rv = make_rsrc((const void*)v_next, v_bytes);
+        k_next += BN * k_row_bytes;
+        v_next += BN * v_row_bytes;
+        k_rows -= BN;
+        v_rows -= BN;
 
         // causal / range mask on the tiles that cross a row's last visible key:
         // key kt + c (c = mb*32 + (i>>2)*8 + lg*4 + (i&3)) is hidden when
