@@ -930,12 +930,16 @@ bool supported_dims(int dqk, int dv) {
     return (dqk == 64 && dv == 64) || (dqk == 128 && dv == 128) || (dqk == 192 && dv == 128);
 }
 
-// Kernel variant for a configuration: query blocks of 32 rows per wave
-// (VPP_NB overrides, for tuning).
-int choose_nb(const vpp_chunk_attn_config_t& c) {
+// Kernel variant for a chunk: query blocks of 32 rows per wave. 64-row waves
+// (NB = 2) unless the chunk is small and its key ranges short (at most two
+// 256-row workgroups per CU, at most 8192 keys per tile on average): there the
+// finer 128-row tiles (NB = 1, two workgroups per CU) even out the unequal
+// key ranges of the diagonal tiles. With dqk = 192 the 32-row variant runs out
+// of registers, so it keeps NB = 2. VPP_NB overrides, for tuning.
+int choose_nb(const vpp_chunk_attn_config_t& c, int64_t tiles256, double mean_keys256) {
     const char* e = getenv("VPP_NB");
     if (e && (atoi(e) == 1 || atoi(e) == 2)) return atoi(e);
-    (void)c;
+    if (c.head_dim_qk <= 128 && tiles256 * c.num_q_heads <= 2 * 256 && mean_keys256 <= 8192.0) return 1;
     return 2;
 }
 
@@ -995,7 +999,14 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
     if (cu_q[num_segments] > c.max_chunk_tokens) return VPP_ERR_INVALID_ARG;
 
     // query tiles of every segment, with their whole key range [0, last position + 1)
-    const int nb = p ? p->nb : choose_nb(c);
+    int64_t tiles256 = 0;
+    double keys256 = 0.0;
+    for (int s = 0; s < num_segments; ++s)
+        for (int r0 = cu_q[s]; r0 < cu_q[s + 1]; r0 += block_rows(2)) {
+            ++tiles256;
+            keys256 += (double)prefix_len[s] + (r0 - cu_q[s]) + std::min(block_rows(2), cu_q[s + 1] - r0);
+        }
+    const int nb = choose_nb(c, tiles256, tiles256 ? keys256 / tiles256 : 0.0);
     const int BM = block_rows(nb);
     std::vector<WorkItem> tiles;
     double pairs = 0.0, key_tiles = 0.0;
@@ -1051,9 +1062,9 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
         p = new (std::nothrow) vpp_chunk_attn_plan_s();
         if (!p) return VPP_ERR_NOMEM;
         p->cfg = c;
-        p->nb = nb;
         *inout_plan = p;
     }
+    p->nb = nb;
     p->scale = c.softmax_scale > 0.f ? c.softmax_scale : (float)(1.0 / sqrt((double)c.head_dim_qk));
     p->items.swap(items);
     p->num_tiles = ntiles;

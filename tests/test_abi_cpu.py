@@ -213,3 +213,23 @@ def test_run_argument_checks_before_any_device_work():
 def test_empty_chunk_plans_to_nothing():
     info = check_plan(cfg(), [0, 0, 0], [0, 5], [3, 0])
     assert info.num_work_items == 0 and info.num_tokens == 0
+
+
+def test_tile_rows_follow_chunk_size(monkeypatch):
+    monkeypatch.delenv("VPP_NB", raising=False)
+    # 4096 rows x 32 heads = 512 workgroups of 256 rows (at most two per CU) with
+    # short key ranges -> 128-row tiles
+    info = check_plan(cfg(hq=32, hkv=8), [0, 4096], [0], [0])
+    assert info.block_m == 128
+    # the same chunk behind a long prefix -> 256-row tiles
+    info = check_plan(cfg(hq=32, hkv=8), [0, 4096], [0], [20480])
+    assert info.block_m == 256
+    # 16384 rows x 32 heads: enough 256-row workgroups
+    info = check_plan(cfg(hq=32, hkv=8, max_tok=16384), [0, 16384], [0], [0])
+    assert info.block_m == 256
+    # dqk = 192 keeps the 64-row waves whatever the size
+    info = check_plan(cfg(hq=8, hkv=8, dqk=192, dv=128), [0, 256], [0], [0])
+    assert info.block_m == 256
+    # every item's rows fit the tile
+    for n in (1, 127, 128, 129, 300):
+        check_plan(cfg(hq=4, hkv=2), [0, n], [0], [17])

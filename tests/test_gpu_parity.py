@@ -228,3 +228,24 @@ def test_packed_equals_per_request():
         o1, l1 = PA.run_chunk(one, q[a + pre[s]:], k, v, [0, n], [a], [pre[s]])
         assert float((op[cu[s]:cu[s + 1]].double() - o1.double()).abs().max()) == 0.0
         assert float((lp[:, cu[s]:cu[s + 1]] - l1).abs().max()) == 0.0
+
+
+@pytest.mark.parametrize("nb", [1, 2])
+@pytest.mark.parametrize("dims", [(64, 64), (128, 128), (192, 128)])
+def test_both_tile_variants(nb, dims, monkeypatch):
+    """Both kernel variants (64-row and 32-row waves), forced, on a ragged packed chunk."""
+    monkeypatch.setenv("VPP_NB", str(nb))
+    dqk, dv = dims
+    hq, hkv = 4, 2
+    segs = [(0, 90, 300), (390, 0, 45), (435, 700, 170)]
+    T = 435 + 700 + 170
+    tok = sum(s[2] for s in segs)
+    std = 1.0 / math.sqrt(dqk)
+    q = _rand((tok, hq, dqk), std, 400 + dqk + nb)
+    k = _rand((T, hkv, dqk), std, 500 + dqk + nb)
+    v = _rand((T, hkv, dv), std, 600 + dqk + nb)
+    cu = np.cumsum([0] + [s[2] for s in segs])
+    attn = _attn(hq, hkv, dqk, dv, tok, T, splits=1)
+    _full_check(attn, q, k, v, cu, [s[0] for s in segs], [s[1] for s in segs],
+                what="nb=%d dims=%s" % (nb, dims))
+    assert attn.info().block_m == 32 * nb * 4
