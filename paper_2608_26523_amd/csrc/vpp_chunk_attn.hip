@@ -683,8 +683,10 @@ void attn_fwd_kernel(AttnArgs a) {
             } else if constexpr (k < A::EXP) {
                 constexpr int nb = k - A::MAXF;
                 const float m = lane_swap32_max(mx[nb]) * a.scale_log2;
-                refresh[nb] = __builtin_amdgcn_ballot_w64(m > m_run[nb] + LAZY_TAU) != 0;
-                const float m_new = refresh[nb] ? fmaxf(m_run[nb], m) : m_run[nb];
+                // per-lane decision: the exps of this row wait only for VALU work;
+                // the wave-wide vote happens once, at the rescale check
+                refresh[nb] = m > m_run[nb] + LAZY_TAU;
+                const float m_new = refresh[nb] ? m : m_run[nb];
                 // a row that has seen no visible key yet (m_new = -inf) has nothing to rescale
                 alpha[nb] = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
                 m_run[nb] = m_new;
@@ -726,9 +728,10 @@ void attn_fwd_kernel(AttnArgs a) {
                     bool any = false;
 #pragma unroll
                     for (int nb = 0; nb < NB; ++nb) any = any || refresh[nb];
-                    if (any) {
+                    if (__builtin_amdgcn_ballot_w64(any) != 0) {
                         // rare: rescale the AGPR accumulators 16 at a time, so the
-                        // branch needs only a few temporary VGPRs
+                        // branch needs only a few temporary VGPRs (alpha = 1 in the
+                        // lanes whose reference did not move)
                         mfma_drain();
                         static_for<NB * DB>([&](auto J) {
                             constexpr int nb = J / DB, d = J % DB;
