@@ -93,6 +93,41 @@ def measured_traffic(workload):
     return None
 
 
+def gemm_reference(dev, n=16384, reps=10):
+    """Rate of the platform's own bf16 GEMM (hipBLASLt through torch.matmul) on operands of
+    the same kind as the attention inputs (i.i.d. normal) and on zeros. MFMA throughput on
+    this part depends on the operand values (power and clock), so this is the ceiling that
+    a dense bf16 contraction reaches here on such data; the published peak is not."""
+    import torch
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    a = torch.randn((n, n), generator=g, device=dev).to(torch.bfloat16)
+    b = torch.randn((n, n), generator=g, device=dev).to(torch.bfloat16)
+
+    def rate(x, y):
+        for _ in range(3):
+            torch.matmul(x, y)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            torch.matmul(x, y)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return 2.0 * n * n * n / (statistics.median(ts) * 1e-3) / 1e12
+
+    r_randn = rate(a, b)
+    z = torch.zeros_like(a)
+    r_zeros = rate(z, z)
+    del a, b, z
+    torch.cuda.empty_cache()
+    return {"library": "hipBLASLt via torch.matmul", "shape": "%dx%dx%d bf16" % (n, n, n),
+            "randn_tflops": round(r_randn, 1), "zeros_tflops": round(r_zeros, 1)}
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -148,6 +183,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=-1)
     ap.add_argument("--workload", default="gqa")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm-ref", action="store_true",
+                    help="skip the library GEMM reference taken after the timed steps")
     ap.add_argument("--chunks", type=int, default=0, help="run only the first N chunks")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, three "
@@ -258,6 +295,10 @@ def main():
                       "tflops": [round(f / (m * 1e-3) / 1e12, 2) for f, m in zip(flops, med)],
                       "splits": splits, "fit": fit, "eq3_residual": eq3},
     }
+    if not args.no_gemm_ref:
+        ref = gemm_reference(dev)
+        ref["attention_frac_of_randn"] = round(achieved / ref["randn_tflops"], 4)
+        res["roofline"]["gemm_ref"] = ref
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, q, k, v, nchunks)
     print(json.dumps(res), flush=True)

@@ -51,6 +51,9 @@ constexpr float LAZY_TAU = 8.0f;
 // The next tiles' global->LDS copies are spread over the first 1/LOAD_SPREAD
 // of a tile's MFMA slots.
 constexpr int LOAD_SPREAD = 2;
+// LDS fragment prefetch distances (in fragments) of the K and V^T operands
+constexpr int K_AHEAD = 3;
+constexpr int V_AHEAD = 2;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -667,8 +670,8 @@ void attn_fwd_kernel(AttnArgs a) {
         }
         float pprev = 0.f;
         bf16x8 pb[NB][2][2];         // [nb][mb][hh]
-        bf16x8 kf[4];                // K fragments in issue order, three in flight
-        bf16x8 vf[3];                // V^T fragments in issue order, two in flight
+        bf16x8 kf[K_AHEAD + 1];      // K fragments in issue order, K_AHEAD in flight
+        bf16x8 vf[V_AHEAD + 1];      // V^T fragments in issue order, V_AHEAD in flight
 
         auto atom = [&](auto K) {
             constexpr int k = decltype(K)::value;
@@ -712,14 +715,16 @@ void attn_fwd_kernel(AttnArgs a) {
             constexpr Sch sch{};
             constexpr int NS = Sch::NS;
             typedef QkCoords<KS, NB> C;
-            // fragments needed first: two V^T fragments, and three K fragments of the next tile
-            vf[0] = load_vfrag(vt_cur, 0, 0, 0);
-            vf[1] = load_vfrag(vt_cur, 0, 0, 1 % DB);
-            if constexpr (has_next) {
-                kf[0] = load_kfrag(kt_nxt, C::ks(0), C::mb(0));
-                kf[1] = load_kfrag(kt_nxt, C::ks(NB), C::mb(NB));
-                kf[2] = load_kfrag(kt_nxt, C::ks(2 * NB), C::mb(2 * NB));
-            }
+            // fragments needed first: V_AHEAD V^T fragments, and K_AHEAD K fragments of the next tile
+            static_for<V_AHEAD>([&](auto I) {
+                constexpr int f = I;
+                vf[f] = load_vfrag(vt_cur, (f / DB) >> 1, (f / DB) & 1, f % DB);
+            });
+            if constexpr (has_next)
+                static_for<K_AHEAD>([&](auto I) {
+                    constexpr int f = I;
+                    kf[f] = load_kfrag(kt_nxt, C::ks(NB * f), C::mb(NB * f));
+                });
             static_for<NS>([&](auto SL) {
                 constexpr int s = SL;
                 constexpr int kind = sch.kind[s];
@@ -757,10 +762,11 @@ void attn_fwd_kernel(AttnArgs a) {
                 } else if constexpr (kind == 0) {
                     constexpr int ks = C::ks(idx), mb = C::mb(idx), nb = C::nb(idx);
                     constexpr int frag = idx / NB;  // (mb, ks) in issue order
-                    // prefetch three fragments ahead with this fragment's first MFMA
-                    if constexpr (nb == 0 && frag + 3 < 2 * KS)
-                        kf[(frag + 3) % 4] = load_kfrag(kt_nxt, C::ks(NB * (frag + 3)), C::mb(NB * (frag + 3)));
-                    const bf16x8 af = kf[frag % 4];
+                    // prefetch K_AHEAD fragments ahead with this fragment's first MFMA
+                    if constexpr (nb == 0 && frag + K_AHEAD < 2 * KS)
+                        kf[(frag + K_AHEAD) % (K_AHEAD + 1)] =
+                            load_kfrag(kt_nxt, C::ks(NB * (frag + K_AHEAD)), C::mb(NB * (frag + K_AHEAD)));
+                    const bf16x8 af = kf[frag % (K_AHEAD + 1)];
                     const bf16x8 bq = qf[nb][ks];
                     if constexpr (ks == 0) MFMA_32x32x16_INIT(s_nxt[mb][nb], af, bq);
                     else MFMA_32x32x16_ACC(s_nxt[mb][nb], af, bq);
@@ -768,12 +774,13 @@ void attn_fwd_kernel(AttnArgs a) {
                     constexpr int grp = idx / (NB * DB), d = (idx / NB) % DB, nb = idx % NB;
                     constexpr int mb = grp >> 1, hh = grp & 1;
                     constexpr int frag = idx / NB;  // (grp, d) in issue order
-                    // prefetch two fragments ahead with this fragment's first MFMA
-                    if constexpr (nb == 0 && frag + 2 < 4 * DB) {
-                        constexpr int f2 = frag + 2;
-                        vf[f2 % 3] = load_vfrag(vt_cur, (f2 / DB) >> 1, (f2 / DB) & 1, f2 % DB);
+                    // prefetch V_AHEAD fragments ahead with this fragment's first MFMA
+                    if constexpr (nb == 0 && frag + V_AHEAD < 4 * DB) {
+                        constexpr int f2 = frag + V_AHEAD;
+                        vf[f2 % (V_AHEAD + 1)] = load_vfrag(vt_cur, (f2 / DB) >> 1, (f2 / DB) & 1, f2 % DB);
                     }
-                    o[d][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[frag % 3], pb[nb][mb][hh], o[d][nb], 0, 0, 0);
+                    o[d][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[frag % (V_AHEAD + 1)], pb[nb][mb][hh],
+                                                                       o[d][nb], 0, 0, 0);
                 }
                 constexpr int a0 = s == 0 ? 0 : sch.atoms_end[s == 0 ? 0 : s - 1];
                 constexpr int a1 = sch.atoms_end[s];

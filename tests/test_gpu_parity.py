@@ -233,7 +233,7 @@ def test_packed_equals_per_request():
 @pytest.mark.parametrize("nb", [1, 2])
 @pytest.mark.parametrize("dims", [(64, 64), (128, 128), (192, 128)])
 def test_both_tile_variants(nb, dims, monkeypatch):
-    """Both kernel variants (64-row and 32-row waves), forced, on a ragged packed chunk."""
+    """Both kernel variants (32-row and 64-row waves), forced, on a ragged packed chunk."""
     monkeypatch.setenv("VPP_NB", str(nb))
     dqk, dv = dims
     hq, hkv = 4, 2
@@ -249,3 +249,22 @@ def test_both_tile_variants(nb, dims, monkeypatch):
     _full_check(attn, q, k, v, cu, [s[0] for s in segs], [s[1] for s in segs],
                 what="nb=%d dims=%s" % (nb, dims))
     assert attn.info().block_m == 32 * nb * 4
+
+
+@pytest.mark.parametrize("nb", [1, 2])
+@pytest.mark.parametrize("dims", [(64, 64), (192, 128)])
+def test_tile_variants_split(nb, dims, monkeypatch):
+    """Both kernel variants with the key range of one ragged request split three ways."""
+    monkeypatch.setenv("VPP_NB", str(nb))
+    dqk, dv = dims
+    hq, hkv = 2, 1
+    prefix, rows = 1000, 300
+    T = prefix + rows
+    std = 1.0 / math.sqrt(dqk)
+    q = _rand((rows, hq, dqk), std, 700 + dqk + nb)
+    k = _rand((T, hkv, dqk), std, 800 + dqk + nb)
+    v = _rand((T, hkv, dv), std, 900 + dqk + nb)
+    cu = np.array([0, rows])
+    attn = _attn(hq, hkv, dqk, dv, rows, T, splits=3)
+    _full_check(attn, q, k, v, cu, [0], [prefix], what="split nb=%d dims=%s" % (nb, dims))
+    assert attn.info().num_splits == 3
