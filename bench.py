@@ -128,6 +128,65 @@ def gemm_reference(dev, n=16384, reps=10):
             "randn_tflops": round(r_randn, 1), "zeros_tflops": round(r_zeros, 1)}
 
 
+def schedule_report(chunk_ms, comm_ms=0.0):
+    """Feed a measured per-chunk latency curve (one layer per virtual stage) to the native
+    model of the pipeline schedules of sections 2.4 and 5.1-5.3: one request alone under
+    each scheme, and two back-to-back copies of it with and without pipelined packing."""
+    from paper_2608_26523_amd import schedule as SC
+    taus = SC.stage_times_from_curve(chunk_ms)
+    out = {"stage_times": "measured per-chunk median latency, one layer per virtual stage",
+           "comm_ms": comm_ms}
+    for name in ("cpp", "vpp", "vpp_async"):
+        r = SC.vpp_sched_simulate([taus], comm_ms, scheme=name)
+        out[name] = {"makespan_ms": round(r["makespan"], 4), "bubble_ratio": round(r["bubble_ratio"], 5),
+                     "idle_ms": [round(x, 4) for x in r["idle"]]}
+    for name in ("vpp_async", "vpp_async_packed"):
+        r = SC.vpp_sched_simulate([taus, taus], comm_ms, scheme=name)
+        out[name + "_2req"] = {"makespan_ms": round(r["makespan"], 4),
+                               "bubble_ratio": round(r["bubble_ratio"], 5),
+                               "request_end_ms": [round(x, 4) for x in r["request_end"]]}
+    return out
+
+
+def schedule_sweep(w, q, k, v, sizes, reps=5):
+    """Per-chunk latency curves of one prompt of the workload at several chunk sizes
+    (the last chunk is shorter when the size does not divide the prompt), each fed to
+    the schedule model: the chunk-size sweep of section 6.1."""
+    import numpy as np
+    import torch
+    from paper_2608_26523_amd.attention import ChunkAttention
+    S = w.seq_len
+    rows = []
+    for C in sizes:
+        attn = ChunkAttention(w.hq, w.hkv, w.dqk, w.dv, max_chunk_tokens=C, max_kv_len=S,
+                              num_splits=w.num_splits)
+        out = torch.empty((C, w.hq, w.dv), dtype=torch.bfloat16, device=q.device)
+        ms = []
+        for c0 in range(0, S, C):
+            n = min(C, S - c0)
+            cu = np.array([0, n], dtype=np.int32)
+            kvs = np.array([0], dtype=np.int64)
+            pre = np.array([c0], dtype=np.int64)
+            attn.plan(cu, kvs, pre)
+            attn.run(q[c0:c0 + n], k, v, out[:n])
+            ts = []
+            for _ in range(reps):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                attn.run(q[c0:c0 + n], k, v, out[:n])
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            ms.append(statistics.median(ts))
+        rep = schedule_report(ms)
+        rows.append({"chunk": C, "chunks": len(ms), "last_chunk_tokens": S - (len(ms) - 1) * C,
+                     "attention_ms": round(sum(ms), 4), "median_ms": [round(x, 4) for x in ms],
+                     "schedule": rep})
+        del attn, out
+    return rows
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -186,6 +245,9 @@ def main():
     ap.add_argument("--no-gemm-ref", action="store_true",
                     help="skip the library GEMM reference taken after the timed steps")
     ap.add_argument("--chunks", type=int, default=0, help="run only the first N chunks")
+    ap.add_argument("--schedule-sweep", default="",
+                    help="comma-separated chunk sizes: time one prompt of the workload at each "
+                         "and print the schedule model's results (one JSON line), nothing else")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, three "
                          "times (the known-size kernel that scales the HBM byte counters)")
@@ -210,6 +272,17 @@ def main():
     from paper_2608_26523_amd.attention import ChunkAttention
 
     w = W.get(args.workload)
+    if args.schedule_sweep:
+        if w.n_requests != 1:
+            print("--schedule-sweep needs a single-request workload", file=sys.stderr)
+            sys.exit(2)
+        dev = torch.device("cuda", 0)
+        torch.cuda.set_device(dev)
+        q, k, v = W.make_inputs(w, dev)
+        sizes = [int(x) for x in args.schedule_sweep.split(",") if x]
+        print(json.dumps({"workload": w.name, "tokens": w.seq_len,
+                          "sweep": schedule_sweep(w, q, k, v, sizes)}), flush=True)
+        return
     steps = args.steps or DEFAULT_STEPS[w.name]
     warmup = args.warmup if args.warmup >= 0 else DEFAULT_WARMUP[w.name]
     dev = torch.device("cuda", 0)
@@ -295,6 +368,8 @@ def main():
                       "tflops": [round(f / (m * 1e-3) / 1e12, 2) for f, m in zip(flops, med)],
                       "splits": splits, "fit": fit, "eq3_residual": eq3},
     }
+    if w.n_requests == 1:
+        res["per_chunk"]["schedule_model"] = schedule_report(med)
     if not args.no_gemm_ref:
         ref = gemm_reference(dev)
         ref["attention_frac_of_randn"] = round(achieved / ref["randn_tflops"], 4)

@@ -1,4 +1,6 @@
-"""Build the HIP library in-tree: hipcc for gfx950 into paper_2608_26523_amd/libvpp_chunk_attn.so."""
+"""Build the native libraries in-tree: the HIP attention library (hipcc for gfx950) into
+paper_2608_26523_amd/libvpp_chunk_attn.so, and the host-only schedule model (g++) into
+paper_2608_26523_amd/libvpp_sched.so."""
 from __future__ import annotations
 
 import os
@@ -10,6 +12,8 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "vpp_chunk_attn.hip")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libvpp_chunk_attn.so")
+SCHED_SRC = os.path.join(PKG, "csrc", "vpp_sched.cpp")
+SCHED_LIB = os.path.join(PKG, "libvpp_sched.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC", "-shared",
@@ -38,5 +42,18 @@ def build(extra_flags=(), out: str = LIB, quiet: bool = True) -> str:
     return out
 
 
+def build_sched(out: str = SCHED_LIB) -> str:
+    """The schedule model is plain host C++: no HIP, so it loads on any machine."""
+    tmp = out + ".tmp"
+    cmd = ["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall", "-Wextra",
+           "-I", INCLUDE, "-o", tmp, SCHED_SRC]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("g++ failed:\n" + res.stdout + res.stderr)
+    os.replace(tmp, out)
+    return out
+
+
 if __name__ == "__main__":
     print(build(quiet=False))
+    print(build_sched())
