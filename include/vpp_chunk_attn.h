@@ -118,6 +118,76 @@ vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t plan,
                                 float* lse, int64_t lse_stride_head,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Paged KV cache. The paper's system runs inside a serving engine (vLLM,
+ * sections 5.4 and 6.1) whose KV cache is cut into fixed-size pages assigned
+ * to requests through block tables; the chunk semantics are unchanged
+ * (section 2.4). Layout (device memory, caller-owned):
+ *   k_pages  bf16 [num_pages][page_size][Hkv][dqk]  strides k_stride_page,
+ *                                                   k_stride_tok, k_stride_head
+ *   v_pages  bf16 [num_pages][page_size][Hkv][dv]   likewise
+ *   block_table int32, row s (segment s of the plan) at block_table +
+ *            s * block_table_stride: entry i is the page holding cache rows
+ *            i*page_size .. (i+1)*page_size - 1 of that segment's request.
+ * The plan's kv_start[s] is the cache row of in-request position 0 (normally
+ * 0) and must be a multiple of 64; cache row j of segment s is row
+ * j % page_size of page block_table[s][j / page_size]. page_size is a power of
+ * two >= 64 (a 64-key tile never straddles a page). The table must cover every
+ * row the chunk reads (kv_start + prefix_len + len rows per segment). Page
+ * indices are clamped to [0, num_pages - 1] on the device, so a bad entry gives
+ * wrong values, never an out-of-range read. Arithmetic, outputs, workspace and
+ * stream semantics are those of vpp_chunk_attn_run, and so are the results:
+ * the same bits as a contiguous cache holding the same rows.
+ * Errors: VPP_ERR_INVALID_ARG for a bad page size, page stride, block table
+ * pointer or kv_start alignment, plus every error of vpp_chunk_attn_run.
+ */
+vpp_status_t vpp_chunk_attn_run_paged(vpp_chunk_attn_plan_t plan,
+                                      const void* q, int64_t q_stride_tok, int64_t q_stride_head,
+                                      const void* k_pages, int64_t k_stride_page, int64_t k_stride_tok,
+                                      int64_t k_stride_head,
+                                      const void* v_pages, int64_t v_stride_page, int64_t v_stride_tok,
+                                      int64_t v_stride_head,
+                                      int32_t page_size, int32_t num_pages,
+                                      const int32_t* block_table, int64_t block_table_stride,
+                                      void* out, int64_t o_stride_tok, int64_t o_stride_head,
+                                      float* lse, int64_t lse_stride_head,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Write a chunk's new keys and values into a paged cache (asynchronously on
+ * `stream`): token t's rows k_new[t] [Hkv][dqk] and v_new[t] [Hkv][dv] go to
+ * slot slot_mapping[t] = page * page_size + row of k_pages / v_pages (layouts
+ * as for vpp_chunk_attn_run_paged). Slots outside [0, num_pages * page_size)
+ * are skipped (e.g. -1 for padding). This is the cache write that must precede
+ * the chunk's attention (section 2.4). Head dims are multiples of 8, at most
+ * 1024; pointers 16-byte aligned (slot_mapping: 8-byte, int64 device array);
+ * strides multiples of 8 elements. Two tokens mapped to one slot race.
+ * Errors: VPP_ERR_INVALID_ARG, VPP_ERR_HIP (launch failure).
+ */
+vpp_status_t vpp_kv_append_paged(const void* k_new, int64_t kn_stride_tok, int64_t kn_stride_head,
+                                 const void* v_new, int64_t vn_stride_tok, int64_t vn_stride_head,
+                                 void* k_pages, int64_t k_stride_page, int64_t k_stride_tok,
+                                 int64_t k_stride_head,
+                                 void* v_pages, int64_t v_stride_page, int64_t v_stride_tok,
+                                 int64_t v_stride_head,
+                                 int32_t num_tokens, int32_t num_kv_heads, int32_t head_dim_qk,
+                                 int32_t head_dim_v, int32_t page_size, int32_t num_pages,
+                                 const int64_t* slot_mapping, void* stream);
+
+/*
+ * Host helper: the slot of each chunk row for vpp_kv_append_paged, from the
+ * same segment metadata as vpp_chunk_attn_plan and a host copy of the block
+ * table (rows of pages_per_row valid entries, block_table_stride apart):
+ * slot_mapping[r] (host, cu_q[n] entries) = page * page_size + row of cache
+ * row kv_start[s] + prefix_len[s] + (r - cu_q[s]). Errors: VPP_ERR_INVALID_ARG
+ * for malformed metadata, a row past its table row, or a negative page.
+ */
+vpp_status_t vpp_paged_slot_mapping(int32_t num_segments, const int32_t* cu_q,
+                                    const int64_t* kv_start, const int64_t* prefix_len,
+                                    const int32_t* block_table, int64_t block_table_stride,
+                                    int32_t pages_per_row, int32_t page_size,
+                                    int64_t* slot_mapping);
+
 /* Free a plan (NULL is ignored). Waits for the device to finish reading its
  * work list first. */
 void vpp_chunk_attn_destroy(vpp_chunk_attn_plan_t plan);

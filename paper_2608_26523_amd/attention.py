@@ -2,7 +2,9 @@
 
 ``ChunkAttention`` validates tensors, owns a plan and a device workspace, and
 passes raw pointers and element strides to ``vpp_chunk_attn_plan`` /
-``vpp_chunk_attn_run``. It does no arithmetic of its own.
+``vpp_chunk_attn_run`` (contiguous cache) or ``vpp_chunk_attn_run_paged`` (paged
+cache); ``kv_append_paged`` wraps ``vpp_kv_append_paged``. Nothing here does
+arithmetic of its own.
 """
 from __future__ import annotations
 
@@ -48,8 +50,9 @@ class ChunkAttention:
         cu = [int(x) for x in cu_q]
         # last cache row the chunk reads: the C ABI cannot see tensor sizes, so the
         # wrapper checks the caches against it before every run
-        self.max_row = max([int(kv_start[s]) + int(prefix_len[s]) + cu[s + 1] - cu[s]
-                            for s in range(len(kv_start)) if cu[s + 1] > cu[s]] or [0])
+        self.seg_rows = [int(kv_start[s]) + int(prefix_len[s]) + cu[s + 1] - cu[s]
+                         for s in range(len(kv_start))]
+        self.max_row = max([self.seg_rows[s] for s in range(len(kv_start)) if cu[s + 1] > cu[s]] or [0])
         if self._ws is None or self._ws.numel() < ws:
             self._ws = torch.empty(ws, dtype=torch.uint8, device=self.device)
         self.tokens = int(cu_q[-1])
@@ -73,31 +76,14 @@ class ChunkAttention:
         if t.stride(-1) != 1:
             raise ValueError("%s: last dimension must be contiguous" % name)
 
-    def run(self, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
-            out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-            stream: Optional[torch.cuda.Stream] = None):
-        """Enqueue the planned chunk on ``stream`` (default: torch's current stream).
-
-        q [tokens, Hq, dqk], k_cache [rows, Hkv, dqk], v_cache [rows, Hkv, dv] bf16;
-        out [tokens, Hq, dv] bf16 (allocated when None); lse an fp32 view whose
-        element [h, r] is chunk row r of head h (e.g. a column slice of a
-        [Hq, seq] tensor), or None.
-        """
+    def _io(self, q: torch.Tensor, out: Optional[torch.Tensor], lse: Optional[torch.Tensor]):
+        """Checks of q, out and lse shared by both run methods; allocates out if None."""
         if self._plan is None:
             raise RuntimeError("plan() must be called before run()")
         c = self.cfg
         self._check(q, "q", torch.bfloat16, 3)
-        self._check(k_cache, "k_cache", torch.bfloat16, 3)
-        self._check(v_cache, "v_cache", torch.bfloat16, 3)
         if q.shape[0] < self.tokens or q.shape[1] != c.num_q_heads or q.shape[2] != c.head_dim_qk:
             raise ValueError("q shape %s does not match the plan" % (tuple(q.shape),))
-        if k_cache.shape[1] != c.num_kv_heads or k_cache.shape[2] != c.head_dim_qk:
-            raise ValueError("k_cache shape %s does not match the config" % (tuple(k_cache.shape),))
-        if v_cache.shape[1] != c.num_kv_heads or v_cache.shape[2] != c.head_dim_v:
-            raise ValueError("v_cache shape %s does not match the config" % (tuple(v_cache.shape),))
-        if k_cache.shape[0] < self.max_row or v_cache.shape[0] < self.max_row:
-            raise ValueError("the planned chunk reads cache rows up to %d but the caches hold "
-                             "%d/%d rows" % (self.max_row, k_cache.shape[0], v_cache.shape[0]))
         if out is None:
             out = torch.empty((self.tokens, c.num_q_heads, c.head_dim_v), dtype=torch.bfloat16,
                               device=q.device)
@@ -111,6 +97,29 @@ class ChunkAttention:
             if lse.shape[0] != c.num_q_heads or lse.shape[1] < self.tokens:
                 raise ValueError("lse shape %s does not match the plan" % (tuple(lse.shape),))
             lse_ptr, lse_sh = lse.data_ptr(), lse.stride(0)
+        return out, lse_ptr, lse_sh
+
+    def run(self, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+            out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+            stream: Optional[torch.cuda.Stream] = None):
+        """Enqueue the planned chunk on ``stream`` (default: torch's current stream).
+
+        q [tokens, Hq, dqk], k_cache [rows, Hkv, dqk], v_cache [rows, Hkv, dv] bf16;
+        out [tokens, Hq, dv] bf16 (allocated when None); lse an fp32 view whose
+        element [h, r] is chunk row r of head h (e.g. a column slice of a
+        [Hq, seq] tensor), or None.
+        """
+        out, lse_ptr, lse_sh = self._io(q, out, lse)
+        c = self.cfg
+        self._check(k_cache, "k_cache", torch.bfloat16, 3)
+        self._check(v_cache, "v_cache", torch.bfloat16, 3)
+        if k_cache.shape[1] != c.num_kv_heads or k_cache.shape[2] != c.head_dim_qk:
+            raise ValueError("k_cache shape %s does not match the config" % (tuple(k_cache.shape),))
+        if v_cache.shape[1] != c.num_kv_heads or v_cache.shape[2] != c.head_dim_v:
+            raise ValueError("v_cache shape %s does not match the config" % (tuple(v_cache.shape),))
+        if k_cache.shape[0] < self.max_row or v_cache.shape[0] < self.max_row:
+            raise ValueError("the planned chunk reads cache rows up to %d but the caches hold "
+                             "%d/%d rows" % (self.max_row, k_cache.shape[0], v_cache.shape[0]))
         s = stream if stream is not None else torch.cuda.current_stream(q.device)
         B.vpp_chunk_attn_run(self._plan,
                              q.data_ptr(), q.stride(0), q.stride(1),
@@ -119,6 +128,44 @@ class ChunkAttention:
                              out.data_ptr(), out.stride(0), out.stride(1),
                              lse_ptr, lse_sh,
                              self._ws.data_ptr(), self._ws.numel(), s.cuda_stream)
+        return out, lse
+
+    def run_paged(self, q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,
+                  block_table: torch.Tensor, out: Optional[torch.Tensor] = None,
+                  lse: Optional[torch.Tensor] = None, stream: Optional[torch.cuda.Stream] = None):
+        """Like ``run`` over a paged cache: k_pages [pages, page_size, Hkv, dqk], v_pages
+        [pages, page_size, Hkv, dv] bf16; block_table int32 [segments, pages_per_row] on the
+        device (row s: the pages of segment s's request, in cache-row order)."""
+        out, lse_ptr, lse_sh = self._io(q, out, lse)
+        c = self.cfg
+        self._check(k_pages, "k_pages", torch.bfloat16, 4)
+        self._check(v_pages, "v_pages", torch.bfloat16, 4)
+        if k_pages.shape[2] != c.num_kv_heads or k_pages.shape[3] != c.head_dim_qk:
+            raise ValueError("k_pages shape %s does not match the config" % (tuple(k_pages.shape),))
+        if v_pages.shape[2] != c.num_kv_heads or v_pages.shape[3] != c.head_dim_v:
+            raise ValueError("v_pages shape %s does not match the config" % (tuple(v_pages.shape),))
+        if k_pages.shape[:2] != v_pages.shape[:2]:
+            raise ValueError("k_pages and v_pages must have the same pages and page size")
+        page = int(k_pages.shape[1])
+        if block_table.dtype != torch.int32 or block_table.dim() != 2 or block_table.device != q.device \
+                or block_table.stride(1) != 1:
+            raise ValueError("block_table must be an int32 [segments, pages] tensor on the GPU")
+        if block_table.shape[0] < len(self.seg_rows):
+            raise ValueError("block_table has %d rows for %d segments" % (block_table.shape[0], len(self.seg_rows)))
+        need = max(self.seg_rows or [0])
+        if need > block_table.shape[1] * page:
+            raise ValueError("the planned chunk reads cache rows up to %d but a block-table row maps "
+                             "%d" % (need, block_table.shape[1] * page))
+        s = stream if stream is not None else torch.cuda.current_stream(q.device)
+        B.vpp_chunk_attn_run_paged(self._plan,
+                                   q.data_ptr(), q.stride(0), q.stride(1),
+                                   k_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1), k_pages.stride(2),
+                                   v_pages.data_ptr(), v_pages.stride(0), v_pages.stride(1), v_pages.stride(2),
+                                   page, int(k_pages.shape[0]),
+                                   block_table.data_ptr(), block_table.stride(0),
+                                   out.data_ptr(), out.stride(0), out.stride(1),
+                                   lse_ptr, lse_sh,
+                                   self._ws.data_ptr(), self._ws.numel(), s.cuda_stream)
         return out, lse
 
     def close(self):
@@ -132,3 +179,30 @@ class ChunkAttention:
             self.close()
         except Exception:
             pass
+
+
+def kv_append_paged(k_new: torch.Tensor, v_new: torch.Tensor, k_pages: torch.Tensor,
+                    v_pages: torch.Tensor, slot_mapping: torch.Tensor,
+                    stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Write k_new [tokens, Hkv, dqk] and v_new [tokens, Hkv, dv] (bf16) into the paged caches
+    at slot_mapping [tokens] (int64, on the GPU; slot = page * page_size + row, -1 skips)."""
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        ChunkAttention._check(t, name, torch.bfloat16, 3)
+    for t, name in ((k_pages, "k_pages"), (v_pages, "v_pages")):
+        ChunkAttention._check(t, name, torch.bfloat16, 4)
+    if slot_mapping.dtype != torch.int64 or slot_mapping.dim() != 1 or slot_mapping.device != k_new.device \
+            or slot_mapping.stride(0) != 1:
+        raise ValueError("slot_mapping must be a contiguous int64 vector on the GPU")
+    T, H, dqk = k_new.shape
+    dv = v_new.shape[2]
+    if v_new.shape[:2] != (T, H) or slot_mapping.shape[0] != T:
+        raise ValueError("k_new, v_new and slot_mapping disagree on tokens/heads")
+    if k_pages.shape[2:] != (H, dqk) or v_pages.shape[2:] != (H, dv) or k_pages.shape[:2] != v_pages.shape[:2]:
+        raise ValueError("page shapes do not match the new rows")
+    s = stream if stream is not None else torch.cuda.current_stream(k_new.device)
+    B.vpp_kv_append_paged(k_new.data_ptr(), k_new.stride(0), k_new.stride(1),
+                          v_new.data_ptr(), v_new.stride(0), v_new.stride(1),
+                          k_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1), k_pages.stride(2),
+                          v_pages.data_ptr(), v_pages.stride(0), v_pages.stride(1), v_pages.stride(2),
+                          T, H, dqk, dv, int(k_pages.shape[1]), int(k_pages.shape[0]),
+                          slot_mapping.data_ptr(), s.cuda_stream)

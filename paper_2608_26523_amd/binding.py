@@ -24,6 +24,7 @@ VPP_ERR_NOMEM = 5
 EXPORTED = [
     "vpp_chunk_attn_plan", "vpp_chunk_attn_run", "vpp_chunk_attn_destroy",
     "vpp_status_str", "vpp_chunk_attn_plan_info", "vpp_chunk_attn_plan_items",
+    "vpp_chunk_attn_run_paged", "vpp_kv_append_paged", "vpp_paged_slot_mapping",
 ]
 
 
@@ -93,6 +94,14 @@ def load(path: Optional[str] = None):
     lib.vpp_chunk_attn_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
     lib.vpp_chunk_attn_plan_items.restype = ctypes.c_int
     lib.vpp_chunk_attn_plan_items.argtypes = [vp, vp, i32, ctypes.POINTER(i32)]
+    lib.vpp_chunk_attn_run_paged.restype = ctypes.c_int
+    lib.vpp_chunk_attn_run_paged.argtypes = [vp, vp, i64, i64, vp, i64, i64, i64, vp, i64, i64, i64,
+                                             i32, i32, vp, i64, vp, i64, i64, vp, i64, vp, sz, vp]
+    lib.vpp_kv_append_paged.restype = ctypes.c_int
+    lib.vpp_kv_append_paged.argtypes = [vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, vp, i64, i64, i64,
+                                        i32, i32, i32, i32, i32, i32, vp, vp]
+    lib.vpp_paged_slot_mapping.restype = ctypes.c_int
+    lib.vpp_paged_slot_mapping.argtypes = [i32, vp, vp, vp, vp, i64, i32, i32, vp]
     if path == LIB_PATH:
         _lib = lib
     return lib
@@ -135,6 +144,50 @@ def vpp_chunk_attn_run(plan: int, q_ptr: int, q_st: int, q_sh: int, k_ptr: int, 
                                    ws_bytes, stream)
     if st != VPP_OK:
         raise VppError(st, "vpp_chunk_attn_run")
+
+
+def vpp_chunk_attn_run_paged(plan: int, q_ptr: int, q_st: int, q_sh: int, k_ptr: int, k_sp: int,
+                             k_st: int, k_sh: int, v_ptr: int, v_sp: int, v_st: int, v_sh: int,
+                             page_size: int, num_pages: int, bt_ptr: int, bt_st: int, out_ptr: int,
+                             o_st: int, o_sh: int, lse_ptr: int, lse_sh: int, ws_ptr: int,
+                             ws_bytes: int, stream: int) -> None:
+    st = load().vpp_chunk_attn_run_paged(plan, q_ptr, q_st, q_sh, k_ptr, k_sp, k_st, k_sh, v_ptr,
+                                         v_sp, v_st, v_sh, page_size, num_pages, bt_ptr, bt_st,
+                                         out_ptr, o_st, o_sh, lse_ptr, lse_sh, ws_ptr, ws_bytes,
+                                         stream)
+    if st != VPP_OK:
+        raise VppError(st, "vpp_chunk_attn_run_paged")
+
+
+def vpp_kv_append_paged(kn_ptr: int, kn_st: int, kn_sh: int, vn_ptr: int, vn_st: int, vn_sh: int,
+                        k_ptr: int, k_sp: int, k_st: int, k_sh: int, v_ptr: int, v_sp: int,
+                        v_st: int, v_sh: int, num_tokens: int, num_kv_heads: int, dqk: int, dv: int,
+                        page_size: int, num_pages: int, slots_ptr: int, stream: int) -> None:
+    st = load().vpp_kv_append_paged(kn_ptr, kn_st, kn_sh, vn_ptr, vn_st, vn_sh, k_ptr, k_sp, k_st,
+                                    k_sh, v_ptr, v_sp, v_st, v_sh, num_tokens, num_kv_heads, dqk,
+                                    dv, page_size, num_pages, slots_ptr, stream)
+    if st != VPP_OK:
+        raise VppError(st, "vpp_kv_append_paged")
+
+
+def vpp_paged_slot_mapping(cu_q: Sequence[int], kv_start: Sequence[int], prefix_len: Sequence[int],
+                           block_table: np.ndarray, page_size: int) -> np.ndarray:
+    """Host slot of every chunk row (int64 [cu_q[-1]]); block_table is a host int32
+    [segments, pages_per_row] array."""
+    cu = _arr(cu_q, np.int32)
+    ks = _arr(kv_start, np.int64)
+    pl = _arr(prefix_len, np.int64)
+    bt = _arr(block_table, np.int32)
+    n = len(ks)
+    if len(cu) != n + 1 or len(pl) != n or bt.ndim != 2 or bt.shape[0] < n:
+        raise ValueError("segment metadata and block table do not match")
+    out = np.zeros(int(cu[-1]) if len(cu) else 0, dtype=np.int64)
+    st = load().vpp_paged_slot_mapping(n, cu.ctypes.data, ks.ctypes.data, pl.ctypes.data,
+                                       bt.ctypes.data, bt.shape[1], bt.shape[1], page_size,
+                                       out.ctypes.data)
+    if st != VPP_OK:
+        raise VppError(st, "vpp_paged_slot_mapping")
+    return out
 
 
 def vpp_chunk_attn_destroy(plan: Optional[int]) -> None:

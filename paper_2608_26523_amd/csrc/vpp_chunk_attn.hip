@@ -114,6 +114,15 @@ struct AttnArgs {
     int32_t tokens;    // chunk rows (partial layout)
     float scale_log2;  // softmax scale * log2(e)
     int32_t xcd_remap;
+    // Paged cache (PAGED kernels only). Cache row j of segment s is row
+    // j & (2^page_shift - 1) of page block_table[s * bt_st + (j >> page_shift)];
+    // the work item's kv_base carries (s << 32) | its first cache row, a multiple
+    // of the key tile, so no tile straddles a page (pages hold >= 64 rows).
+    const int32_t* block_table;
+    int64_t bt_st;
+    int64_t k_sp, v_sp;  // element strides between pages
+    int32_t page_shift;
+    int32_t num_pages;   // page indices are clamped below it
 };
 
 // LDS tiles: K [BN][DQK] and V [BN][DV] bf16, row-major in 16-byte granules,
@@ -428,7 +437,7 @@ __device__ __forceinline__ void static_range(F&& f) {
 // NB = 2: 64 query rows per wave, one workgroup (4 waves) per CU. NB = 1: 32
 // rows per wave and half the registers, so two workgroups share a CU and each
 // SIMD interleaves two waves' instruction streams.
-template <int DQK, int DV, int NB, bool SPLIT>
+template <int DQK, int DV, int NB, bool SPLIT, bool PAGED>
 __global__ __attribute__((amdgpu_flat_work_group_size(NTHREADS, NTHREADS), amdgpu_waves_per_eu(3 - NB, 3 - NB)))
 void attn_fwd_kernel(AttnArgs a) {
     typedef Tiles<DQK, DV, NB> T;
@@ -465,9 +474,29 @@ void attn_fwd_kernel(AttnArgs a) {
     const int lg = lane >> 5;
 
     const int kb = it.key_begin, ke = it.key_end;
-    const u16* kbase = a.k + it.kv_base * a.k_st + (int64_t)hk * a.k_sh;
-    const u16* vbase = a.v + it.kv_base * a.v_st + (int64_t)hk * a.v_sh;
+    // contiguous cache: the request's row 0 of head hk; paged: page 0's row 0
+    const int64_t cache_row0 = PAGED ? 0 : it.kv_base;
+    const u16* kbase = a.k + cache_row0 * a.k_st + (int64_t)hk * a.k_sh;
+    const u16* vbase = a.v + cache_row0 * a.v_st + (int64_t)hk * a.v_sh;
     const int ntiles = (ke - kb + BN - 1) / BN;
+    // paged cache: this segment's block-table row and the cache row of key 0
+    const int32_t* bt_row = PAGED ? a.block_table + (int64_t)(int32_t)(it.kv_base >> 32) * a.bt_st : nullptr;
+    const int kv_off = PAGED ? (int)(uint32_t)it.kv_base : 0;
+    const int pmask = PAGED ? (1 << a.page_shift) - 1 : 0;
+    const int last_row = kv_off + ke - 1;  // page reads past the key range are clamped here
+    auto clamp_page = [&](int pg) { return (int)min((uint32_t)pg, (uint32_t)(a.num_pages - 1)); };
+    auto page_of = [&](int row) {  // synchronous lookup (prologue)
+        return clamp_page(__builtin_amdgcn_readfirstlane(bt_row[min(row, last_row) >> a.page_shift]));
+    };
+    // first element of the tile of keys starting at kt
+    auto tile_src = [&](const u16* base, int64_t page_st, int64_t row_st, int kt) -> const u16* {
+        if constexpr (PAGED) {
+            const int row = kv_off + kt;
+            return base + (int64_t)page_of(row) * page_st + (int64_t)(row & pmask) * row_st;
+        } else {
+            return base + (int64_t)kt * row_st;
+        }
+    };
 
     // This lane's NB query rows (one per 32-column block of S^T), as B
     // operands in AGPRs. Rows past the tile re-read its last row (their results
@@ -505,10 +534,10 @@ void attn_fwd_kernel(AttnArgs a) {
     }
     // resources over the rows [kt, min(kt + BN, ke)) (none when kt >= ke)
     auto k_rsrc = [&](int kt) {
-        return make_rsrc(kbase + (int64_t)kt * a.k_st, max(0, min(BN, ke - kt)) * (int)a.k_st * 2);
+        return make_rsrc(tile_src(kbase, a.k_sp, a.k_st, kt), max(0, min(BN, ke - kt)) * (int)a.k_st * 2);
     };
     auto v_rsrc = [&](int kt) {
-        return make_rsrc(vbase + (int64_t)kt * a.v_st, max(0, min(BN, ke - kt)) * (int)a.v_st * 2);
+        return make_rsrc(tile_src(vbase, a.v_sp, a.v_st, kt), max(0, min(BN, ke - kt)) * (int)a.v_st * 2);
     };
     const uint32_t lds_wave = (uint32_t)(uintptr_t)(lds_void_t*)smem + (uint32_t)wave * 1024u;
     // copy t of the K (V) tile into buffer B: LDS offset from this wave's base
@@ -606,9 +635,18 @@ void attn_fwd_kernel(AttnArgs a) {
     // Running sources of the copies a step issues (K(t+2) and V(t+1)): scalar
     // pointer and remaining row count, advanced by one tile per step.
     const int k_row_bytes = (int)a.k_st * 2, v_row_bytes = (int)a.v_st * 2;
-    uint64_t k_next = (uint64_t)(uintptr_t)(kbase + (int64_t)(kb + 2 * BN) * a.k_st);
-    uint64_t v_next = (uint64_t)(uintptr_t)(vbase + (int64_t)(kb + BN) * a.v_st);
+    uint64_t k_next = PAGED ? 0 : (uint64_t)(uintptr_t)(kbase + (int64_t)(kb + 2 * BN) * a.k_st);
+    uint64_t v_next = PAGED ? 0 : (uint64_t)(uintptr_t)(vbase + (int64_t)(kb + BN) * a.v_st);
     int k_rows = ke - kb - 2 * BN, v_rows = ke - kb - BN;
+    // paged cache: the page of the K tile a step copies is read one step ahead
+    // (raw, clamped at its use), and V(t+1) shares K(t+1)'s page
+    int pg_pending = 0, pg_prev = 0;
+    if constexpr (PAGED) {
+        if (ntiles > 0) {
+            pg_prev = page_of(kv_off + kb + BN);
+            pg_pending = bt_row[min(kv_off + kb + 2 * BN, last_row) >> a.page_shift];
+        }
+    }
 
     // One key tile: mask S(t) if needed, then the scheduled mix of S(t+1)
     // MFMAs, the softmax of S(t) and the O^T += V^T P^T MFMAs of tile t.
@@ -625,12 +663,26 @@ void attn_fwd_kernel(AttnArgs a) {
         // the last tile the resources are empty: the copies then only write
         // zeros into buffers that no later step reads, and the step needs no
         // branch around them.
+        if constexpr (PAGED) {
+            // the page read during the previous step is complete after the
+            // barrier; the empty asm pins its use here, before any LDS read of
+            // this step is in flight
+            int pg_k = clamp_page(__builtin_amdgcn_readfirstlane(pg_pending));
+            asm volatile("" : "+s"(pg_k) : : "memory");
+            const int row_k = kv_off + kt + 2 * BN;
+            k_next = (uint64_t)(uintptr_t)(kbase + (int64_t)pg_k * a.k_sp + (int64_t)(row_k & pmask) * a.k_st);
+            v_next = (uint64_t)(uintptr_t)(vbase + (int64_t)pg_prev * a.v_sp + (int64_t)((row_k - BN) & pmask) * a.v_st);
+            pg_prev = pg_k;
+            pg_pending = bt_row[min(row_k + BN, last_row) >> a.page_shift];
+        }
         const int k_bytes = k_rows >= BN ? BN * k_row_bytes : (k_rows > 0 ? k_rows * k_row_bytes : 0);
         const int v_bytes = v_rows >= BN ? BN * v_row_bytes : (v_rows > 0 ? v_rows * v_row_bytes : 0);
         const i32x4 rk = make_rsrc((const void*)k_next, k_bytes);
         const i32x4 rv = make_rsrc((const void*)v_next, v_bytes);
-        k_next += BN * k_row_bytes;
-        v_next += BN * v_row_bytes;
+        if constexpr (!PAGED) {
+            k_next += BN * k_row_bytes;
+            v_next += BN * v_row_bytes;
+        }
         k_rows -= BN;
         v_rows -= BN;
 
@@ -914,10 +966,52 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // ---------------------------------------------------------------------------
 // host side: plan
 // ---------------------------------------------------------------------------
+// Scatter of a chunk's new K/V rows into a paged cache: the write that puts a
+// chunk's own keys and values in the cache before its attention (section 2.4).
+// One thread moves one 16-byte granule; consecutive threads walk the granules
+// of one (token, head) row, K first, so reads and writes are contiguous runs.
+// slot = page * page_size + row; slots outside [0, num_pages * page_size) are
+// skipped (padding tokens use -1).
+struct AppendArgs {
+    const u16* k_new;
+    const u16* v_new;
+    u16* k_pages;
+    u16* v_pages;
+    const int64_t* slots;
+    int64_t kn_st, kn_sh, vn_st, vn_sh;  // element strides
+    int64_t k_sp, k_st, k_sh, v_sp, v_st, v_sh;
+    int32_t tokens, heads, k_gran, v_gran, page_shift, num_pages;
+};
+
+__global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
+    const int per = a.k_gran + a.v_gran;  // granules per (token, head)
+    const int gid = (int)(blockIdx.x * 256u + threadIdx.x);
+    if (gid >= a.tokens * a.heads * per) return;
+    const int g = gid % per;
+    const int th = gid / per;
+    const int h = th % a.heads;
+    const int t = th / a.heads;
+    const int64_t slot = a.slots[t];
+    if (slot < 0 || slot >= ((int64_t)a.num_pages << a.page_shift)) return;
+    const int64_t page = slot >> a.page_shift;
+    const int64_t row = slot & (((int64_t)1 << a.page_shift) - 1);
+    if (g < a.k_gran) {
+        const uint4* src = (const uint4*)(a.k_new + (int64_t)t * a.kn_st + (int64_t)h * a.kn_sh) + g;
+        uint4* dst = (uint4*)(a.k_pages + page * a.k_sp + row * a.k_st + (int64_t)h * a.k_sh) + g;
+        *dst = *src;
+    } else {
+        const int gv = g - a.k_gran;
+        const uint4* src = (const uint4*)(a.v_new + (int64_t)t * a.vn_st + (int64_t)h * a.vn_sh) + gv;
+        uint4* dst = (uint4*)(a.v_pages + page * a.v_sp + row * a.v_st + (int64_t)h * a.v_sh) + gv;
+        *dst = *src;
+    }
+}
+
 struct vpp_chunk_attn_plan_s {
     vpp_chunk_attn_config_t cfg;
     float scale;
     std::vector<WorkItem> items;
+    std::vector<int32_t> item_seg;  // segment of each work item (paged runs)
     int32_t num_tiles = 0;
     int32_t num_splits = 1;
     int32_t nb = 2;  // 32-row query blocks per wave of the kernel variant the plan was made for
@@ -1019,6 +1113,7 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
     const int nb = choose_nb(c, tiles256, tiles256 ? keys256 / tiles256 : 0.0);
     const int BM = block_rows(nb);
     std::vector<WorkItem> tiles;
+    std::vector<int32_t> tile_seg;
     double pairs = 0.0, key_tiles = 0.0;
     try {
         for (int s = 0; s < num_segments; ++s) {
@@ -1032,6 +1127,7 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
                 w.split = 0;
                 w.kv_base = kv_start[s];
                 tiles.push_back(w);
+                tile_seg.push_back(s);
                 // visible pairs: sum over rows of (position + 1)
                 pairs += (double)w.nrows * (double)w.pos0 + 0.5 * (double)w.nrows * (w.nrows + 1);
                 key_tiles += ceil((double)w.key_end / BN);
@@ -1044,9 +1140,12 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
     const int nsplit = ntiles ? choose_splits(c, ntiles, key_tiles / ntiles) : 1;
 
     std::vector<WorkItem> items;
+    std::vector<int32_t> iseg;
     try {
         items.reserve((size_t)ntiles * nsplit);
-        for (const WorkItem& t : tiles) {
+        iseg.reserve((size_t)ntiles * nsplit);
+        for (size_t ti = 0; ti < tiles.size(); ++ti) {
+            const WorkItem& t = tiles[ti];
             const int nkt = (t.key_end + BN - 1) / BN;
             for (int sp = 0; sp < nsplit; ++sp) {
                 WorkItem w = t;
@@ -1058,15 +1157,26 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
                     w.key_begin = std::min(w.key_begin, w.key_end);
                 }
                 items.push_back(w);
+                iseg.push_back(tile_seg[ti]);
             }
         }
+        // longest key range first, so the short ones fill the tail of the launch
+        std::vector<int32_t> order(items.size());
+        for (size_t i = 0; i < order.size(); ++i) order[i] = (int32_t)i;
+        std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
+            return (items[x].key_end - items[x].key_begin) > (items[y].key_end - items[y].key_begin);
+        });
+        std::vector<WorkItem> sorted(items.size());
+        std::vector<int32_t> sorted_seg(items.size());
+        for (size_t i = 0; i < order.size(); ++i) {
+            sorted[i] = items[order[i]];
+            sorted_seg[i] = iseg[order[i]];
+        }
+        items.swap(sorted);
+        iseg.swap(sorted_seg);
     } catch (const std::bad_alloc&) {
         return VPP_ERR_NOMEM;
     }
-    // longest key range first, so the short ones fill the tail of the launch
-    std::stable_sort(items.begin(), items.end(), [](const WorkItem& x, const WorkItem& y) {
-        return (x.key_end - x.key_begin) > (y.key_end - y.key_begin);
-    });
 
     if (!p) {
         p = new (std::nothrow) vpp_chunk_attn_plan_s();
@@ -1077,6 +1187,7 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
     p->nb = nb;
     p->scale = c.softmax_scale > 0.f ? c.softmax_scale : (float)(1.0 / sqrt((double)c.head_dim_qk));
     p->items.swap(items);
+    p->item_seg.swap(iseg);
     p->num_tiles = ntiles;
     p->num_splits = nsplit;
     p->tokens = cu_q[num_segments];
@@ -1146,23 +1257,35 @@ namespace {
 bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 bool stride_ok(int64_t s) { return s > 0 && (s % 8) == 0; }
 
-template <int DQK, int DV, int NB>
+template <int DQK, int DV, int NB, bool PAGED>
 hipError_t launch(const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
     const int64_t total = (int64_t)a.num_items * a.num_heads;
     if (total <= 0) return hipSuccess;
     if (total > (int64_t)INT32_MAX) return hipErrorInvalidValue;
     dim3 grid((unsigned)total), block(NTHREADS);
     if (split) {
-        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, true>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, true, PAGED>), grid, block, 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int64_t threads = (int64_t)ca.tokens * ca.num_heads * (DV / 4);
         dim3 cg((unsigned)((threads + 255) / 256));
         hipLaunchKernelGGL((combine_kernel<DV>), cg, dim3(256), 0, stream, ca);
     } else {
-        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, false>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, false, PAGED>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
+}
+
+template <bool PAGED>
+hipError_t launch_dims(int nb, int dqk, const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
+    if (nb == 1) {
+        if (dqk == 64) return launch<64, 64, 1, PAGED>(a, split, ca, stream);
+        if (dqk == 128) return launch<128, 128, 1, PAGED>(a, split, ca, stream);
+        return launch<192, 128, 1, PAGED>(a, split, ca, stream);
+    }
+    if (dqk == 64) return launch<64, 64, 2, PAGED>(a, split, ca, stream);
+    if (dqk == 128) return launch<128, 128, 2, PAGED>(a, split, ca, stream);
+    return launch<192, 128, 2, PAGED>(a, split, ca, stream);
 }
 
 int env_xcd_remap() {
@@ -1172,11 +1295,19 @@ int env_xcd_remap() {
 
 }  // namespace
 
-extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int64_t q_sh,
-                                           const void* k, int64_t k_st, int64_t k_sh, const void* v,
-                                           int64_t v_st, int64_t v_sh, void* out, int64_t o_st, int64_t o_sh,
-                                           float* lse, int64_t lse_sh, void* workspace, size_t workspace_bytes,
-                                           void* stream_ptr) {
+namespace {
+
+// Paged-cache description of one run (see vpp_chunk_attn_run_paged).
+struct PagedKV {
+    const int32_t* block_table;
+    int64_t bt_st, k_sp, v_sp;
+    int32_t page_shift, num_pages;
+};
+
+vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int64_t q_sh, const void* k,
+                      int64_t k_st, int64_t k_sh, const void* v, int64_t v_st, int64_t v_sh, void* out,
+                      int64_t o_st, int64_t o_sh, float* lse, int64_t lse_sh, void* workspace,
+                      size_t workspace_bytes, void* stream_ptr, const PagedKV* pg) {
     if (!p) return VPP_ERR_INVALID_ARG;
     if (!q || !k || !v || !out) return VPP_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return VPP_ERR_INVALID_ARG;
@@ -1214,6 +1345,11 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
         p->staging_cap[slot] = p->items_bytes;
     }
     memcpy(p->staging[slot], p->items.data(), p->items_bytes);
+    if (pg) {
+        // paged: the kernel finds the segment's block-table row from kv_base
+        for (size_t i = 0; i < p->items.size(); ++i)
+            p->staging[slot][i].kv_base = ((int64_t)p->item_seg[i] << 32) | p->items[i].kv_base;
+    }
     char* ws = (char*)workspace;
     if (hipMemcpyAsync(ws, p->staging[slot], p->items_bytes, hipMemcpyHostToDevice, stream) != hipSuccess)
         return VPP_ERR_HIP;
@@ -1238,6 +1374,14 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
     a.tokens = p->tokens;
     a.scale_log2 = (float)((double)p->scale * 1.4426950408889634);
     a.xcd_remap = env_xcd_remap();
+    if (pg) {
+        a.block_table = pg->block_table;
+        a.bt_st = pg->bt_st;
+        a.k_sp = pg->k_sp;
+        a.v_sp = pg->v_sp;
+        a.page_shift = pg->page_shift;
+        a.num_pages = pg->num_pages;
+    }
     const bool split = p->num_splits > 1;
     CombineArgs ca;
     memset(&ca, 0, sizeof ca);
@@ -1255,15 +1399,106 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
         ca.num_heads = c.num_q_heads;
         ca.splits = p->num_splits;
     }
-    hipError_t e;
-    if (p->nb == 1) {
-        if (c.head_dim_qk == 64) e = launch<64, 64, 1>(a, split, ca, stream);
-        else if (c.head_dim_qk == 128) e = launch<128, 128, 1>(a, split, ca, stream);
-        else e = launch<192, 128, 1>(a, split, ca, stream);
-    } else {
-        if (c.head_dim_qk == 64) e = launch<64, 64, 2>(a, split, ca, stream);
-        else if (c.head_dim_qk == 128) e = launch<128, 128, 2>(a, split, ca, stream);
-        else e = launch<192, 128, 2>(a, split, ca, stream);
-    }
+    const hipError_t e = pg ? launch_dims<true>(p->nb, c.head_dim_qk, a, split, ca, stream)
+                            : launch_dims<false>(p->nb, c.head_dim_qk, a, split, ca, stream);
     return e == hipSuccess ? VPP_OK : VPP_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int64_t q_sh,
+                                           const void* k, int64_t k_st, int64_t k_sh, const void* v,
+                                           int64_t v_st, int64_t v_sh, void* out, int64_t o_st, int64_t o_sh,
+                                           float* lse, int64_t lse_sh, void* workspace, size_t workspace_bytes,
+                                           void* stream_ptr) {
+    return run_impl(p, q, q_st, q_sh, k, k_st, k_sh, v, v_st, v_sh, out, o_st, o_sh, lse, lse_sh, workspace,
+                    workspace_bytes, stream_ptr, nullptr);
+}
+
+extern "C" vpp_status_t vpp_chunk_attn_run_paged(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st,
+                                                 int64_t q_sh, const void* k_pages, int64_t k_sp, int64_t k_st,
+                                                 int64_t k_sh, const void* v_pages, int64_t v_sp, int64_t v_st,
+                                                 int64_t v_sh, int32_t page_size, int32_t num_pages,
+                                                 const int32_t* block_table, int64_t bt_st, void* out,
+                                                 int64_t o_st, int64_t o_sh, float* lse, int64_t lse_sh,
+                                                 void* workspace, size_t workspace_bytes, void* stream_ptr) {
+    if (!p || !block_table || ((uintptr_t)block_table & 3u) != 0) return VPP_ERR_INVALID_ARG;
+    if (page_size < BN || page_size > (1 << 20) || (page_size & (page_size - 1)) != 0) return VPP_ERR_INVALID_ARG;
+    if (num_pages < 1 || bt_st < 0) return VPP_ERR_INVALID_ARG;
+    // pages start on 16-byte boundaries, and one page's rows fit the kernels' 32-bit row offsets
+    if (!stride_ok(k_sp) || !stride_ok(v_sp) || k_sp < 1 || v_sp < 1) return VPP_ERR_INVALID_ARG;
+    if ((int64_t)page_size * k_st >= ((int64_t)1 << 31) || (int64_t)page_size * v_st >= ((int64_t)1 << 31))
+        return VPP_ERR_INVALID_ARG;
+    for (size_t i = 0; i < p->items.size(); ++i)
+        if (p->items[i].kv_base % BN != 0 || p->items[i].kv_base >= ((int64_t)1 << 31))
+            return VPP_ERR_INVALID_ARG;  // a key tile must not straddle two pages
+    int shift = 0;
+    while ((1 << shift) < page_size) ++shift;
+    PagedKV pg{block_table, bt_st, k_sp, v_sp, shift, num_pages};
+    return run_impl(p, q, q_st, q_sh, k_pages, k_st, k_sh, v_pages, v_st, v_sh, out, o_st, o_sh, lse, lse_sh,
+                    workspace, workspace_bytes, stream_ptr, &pg);
+}
+
+extern "C" vpp_status_t vpp_kv_append_paged(const void* k_new, int64_t kn_st, int64_t kn_sh, const void* v_new,
+                                            int64_t vn_st, int64_t vn_sh, void* k_pages, int64_t k_sp,
+                                            int64_t k_st, int64_t k_sh, void* v_pages, int64_t v_sp, int64_t v_st,
+                                            int64_t v_sh, int32_t num_tokens, int32_t num_kv_heads,
+                                            int32_t head_dim_qk, int32_t head_dim_v, int32_t page_size,
+                                            int32_t num_pages, const int64_t* slot_mapping, void* stream_ptr) {
+    if (num_tokens < 0 || num_kv_heads < 1 || num_pages < 1) return VPP_ERR_INVALID_ARG;
+    if (head_dim_qk < 8 || head_dim_v < 8 || head_dim_qk % 8 || head_dim_v % 8 || head_dim_qk > 1024 ||
+        head_dim_v > 1024)
+        return VPP_ERR_INVALID_ARG;
+    if (page_size < BN || page_size > (1 << 20) || (page_size & (page_size - 1)) != 0) return VPP_ERR_INVALID_ARG;
+    if (num_tokens == 0) return VPP_OK;
+    if (!k_new || !v_new || !k_pages || !v_pages || !slot_mapping) return VPP_ERR_INVALID_ARG;
+    if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pages) || !aligned16(v_pages) ||
+        ((uintptr_t)slot_mapping & 7u) != 0)
+        return VPP_ERR_INVALID_ARG;
+    const int64_t st[] = {kn_st, kn_sh, vn_st, vn_sh, k_sp, k_st, k_sh, v_sp, v_st, v_sh};
+    for (int64_t x : st)
+        if (!stride_ok(x)) return VPP_ERR_INVALID_ARG;
+    const int64_t total = (int64_t)num_tokens * num_kv_heads * ((head_dim_qk + head_dim_v) / 8);
+    if (total >= ((int64_t)1 << 31) - 256) return VPP_ERR_INVALID_ARG;
+    AppendArgs a;
+    a.k_new = (const u16*)k_new;
+    a.v_new = (const u16*)v_new;
+    a.k_pages = (u16*)k_pages;
+    a.v_pages = (u16*)v_pages;
+    a.slots = slot_mapping;
+    a.kn_st = kn_st; a.kn_sh = kn_sh; a.vn_st = vn_st; a.vn_sh = vn_sh;
+    a.k_sp = k_sp; a.k_st = k_st; a.k_sh = k_sh; a.v_sp = v_sp; a.v_st = v_st; a.v_sh = v_sh;
+    a.tokens = num_tokens;
+    a.heads = num_kv_heads;
+    a.k_gran = head_dim_qk / 8;
+    a.v_gran = head_dim_v / 8;
+    int shift = 0;
+    while ((1 << shift) < page_size) ++shift;
+    a.page_shift = shift;
+    a.num_pages = num_pages;
+    hipLaunchKernelGGL(kv_append_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                       (hipStream_t)stream_ptr, a);
+    return hipGetLastError() == hipSuccess ? VPP_OK : VPP_ERR_HIP;
+}
+
+extern "C" vpp_status_t vpp_paged_slot_mapping(int32_t num_segments, const int32_t* cu_q, const int64_t* kv_start,
+                                               const int64_t* prefix_len, const int32_t* block_table,
+                                               int64_t block_table_stride, int32_t pages_per_row,
+                                               int32_t page_size, int64_t* slot_mapping) {
+    if (num_segments < 0 || !cu_q || page_size < 1 || pages_per_row < 0 || block_table_stride < 0)
+        return VPP_ERR_INVALID_ARG;
+    if (num_segments == 0) return VPP_OK;
+    if (!kv_start || !prefix_len || !block_table || !slot_mapping || cu_q[0] != 0) return VPP_ERR_INVALID_ARG;
+    for (int s = 0; s < num_segments; ++s) {
+        if (cu_q[s + 1] < cu_q[s] || kv_start[s] < 0 || prefix_len[s] < 0) return VPP_ERR_INVALID_ARG;
+        for (int r = cu_q[s]; r < cu_q[s + 1]; ++r) {
+            const int64_t row = kv_start[s] + prefix_len[s] + (r - cu_q[s]);
+            const int64_t idx = row / page_size;
+            if (idx >= pages_per_row) return VPP_ERR_INVALID_ARG;
+            const int32_t pg = block_table[(int64_t)s * block_table_stride + idx];
+            if (pg < 0) return VPP_ERR_INVALID_ARG;
+            slot_mapping[r] = (int64_t)pg * page_size + row % page_size;
+        }
+    }
+    return VPP_OK;
 }
