@@ -187,6 +187,54 @@ def schedule_sweep(w, q, k, v, sizes, reps=5):
     return rows
 
 
+def build_paged(w, k, v, segs, page, seed=0):
+    """Copy the workload's cache into pages of `page` rows, each request's pages in a
+    random order, and the per-chunk block tables (one row per segment, in the order of
+    the chunk's segments) and slot mappings (where the chunk's own rows go)."""
+    import numpy as np
+    import torch
+    from paper_2608_26523_amd import binding as B
+    rng = np.random.default_rng(seed)
+    req_rows = {}
+    for (_, cu, kvs, pre) in segs:
+        for s in range(len(kvs)):
+            r = int(kvs[s])
+            req_rows[r] = max(req_rows.get(r, 0), int(pre[s]) + int(cu[s + 1] - cu[s]))
+    starts = sorted(req_rows)
+    npg = {r: (req_rows[r] + page - 1) // page for r in starts}
+    total = sum(npg.values())
+    perm = rng.permutation(total).astype(np.int32)
+    hkv, dqk, dv = k.shape[1], k.shape[2], v.shape[2]
+    k_pages = torch.zeros((total, page, hkv, dqk), dtype=k.dtype, device=k.device)
+    v_pages = torch.zeros((total, page, hkv, dv), dtype=v.dtype, device=v.device)
+    table, pos = {}, 0
+    for r in starts:
+        ids = perm[pos:pos + npg[r]]
+        pos += npg[r]
+        table[r] = ids
+        rows = req_rows[r]
+        full = rows // page
+        idx = torch.as_tensor(ids[:full].astype(np.int64), device=k.device)
+        if full:
+            k_pages.index_copy_(0, idx, k[r:r + full * page].reshape(full, page, hkv, dqk))
+            v_pages.index_copy_(0, idx, v[r:r + full * page].reshape(full, page, hkv, dv))
+        rem = rows - full * page
+        if rem:
+            k_pages[int(ids[full]), :rem] = k[r + full * page:r + rows]
+            v_pages[int(ids[full]), :rem] = v[r + full * page:r + rows]
+    per_chunk = []
+    for (_, cu, kvs, pre) in segs:
+        width = max(npg[int(x)] for x in kvs)
+        bt = np.zeros((len(kvs), width), dtype=np.int32)
+        for s in range(len(kvs)):
+            ids = table[int(kvs[s])]
+            bt[s, :len(ids)] = ids
+            bt[s, len(ids):] = ids[0]
+        slots = B.vpp_paged_slot_mapping(cu, [0] * len(kvs), pre, bt, page)
+        per_chunk.append((torch.as_tensor(bt, device=k.device), torch.as_tensor(slots, device=k.device)))
+    return k_pages, v_pages, per_chunk
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -245,6 +293,9 @@ def main():
     ap.add_argument("--no-gemm-ref", action="store_true",
                     help="skip the library GEMM reference taken after the timed steps")
     ap.add_argument("--chunks", type=int, default=0, help="run only the first N chunks")
+    ap.add_argument("--paged", type=int, default=0,
+                    help="page size: run the path over a paged KV cache (pages in random order); "
+                         "each chunk first appends its own K/V rows into its pages, then attends")
     ap.add_argument("--schedule-sweep", default="",
                     help="comma-separated chunk sizes: time one prompt of the workload at each "
                          "and print the schedule model's results (one JSON line), nothing else")
@@ -300,15 +351,33 @@ def main():
     flops = [chunk_flops(w, cu, pre)[0] for (_, cu, _, pre) in segs]
     nbytes = [chunk_bytes(w, cu, pre) for (_, cu, _, pre) in segs]
     stream = torch.cuda.current_stream(dev)
+    paged = None
+    if args.paged:
+        from paper_2608_26523_amd.attention import kv_append_paged
+        paged = build_paged(w, k, v, segs, args.paged)
+        append_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(nchunks)]
 
     def step(events=None):
         for c, (t0, cu, kvs, pre) in enumerate(segs):
             a = attn[c]
-            a.plan(cu, kvs, pre)
             tok = int(cu[-1])
-            if events is not None:
-                events[c][0].record(stream)
-            a.run(q[t0:t0 + tok], k, v, out[t0:t0 + tok], lse[:, t0:t0 + tok], stream=stream)
+            if paged is None:
+                a.plan(cu, kvs, pre)
+                if events is not None:
+                    events[c][0].record(stream)
+                a.run(q[t0:t0 + tok], k, v, out[t0:t0 + tok], lse[:, t0:t0 + tok], stream=stream)
+            else:
+                k_pages, v_pages, per_chunk = paged
+                bt, slots = per_chunk[c]
+                a.plan(cu, [0] * len(kvs), pre)
+                if events is not None:
+                    append_ev[c][0].record(stream)
+                kv_append_paged(k[t0:t0 + tok], v[t0:t0 + tok], k_pages, v_pages, slots, stream=stream)
+                if events is not None:
+                    append_ev[c][1].record(stream)
+                    events[c][0].record(stream)
+                a.run_paged(q[t0:t0 + tok], k_pages, v_pages, bt, out[t0:t0 + tok], lse[:, t0:t0 + tok],
+                            stream=stream)
             if events is not None:
                 events[c][1].record(stream)
 
@@ -360,14 +429,24 @@ def main():
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic(w.name),
+                     "traffic": None if args.paged else measured_traffic(w.name),
                      "kernel": "attn_fwd_kernel", "avg_launch_ms": round(kernel_ms, 4),
                      "flops_per_launch": total_flops / nchunks,
                      "algorithmic_bytes_per_launch": sum(nbytes) / nchunks},
+        "kv_cache": ("paged, %d-row pages in random order; each chunk appends its K/V first" % args.paged
+                     if args.paged else "contiguous"),
         "per_chunk": {"prefix_tokens": prefix, "median_ms": [round(x, 4) for x in med],
                       "tflops": [round(f / (m * 1e-3) / 1e12, 2) for f, m in zip(flops, med)],
                       "splits": splits, "fit": fit, "eq3_residual": eq3},
     }
+    if paged is not None:
+        # the last timed step's append kernels: HBM-bound, new K/V rows read and written once
+        app_ms = [append_ev[c][0].elapsed_time(append_ev[c][1]) for c in range(nchunks)]
+        app_bytes = [2 * int(cu[-1]) * w.hkv * (w.dqk + w.dv) * 2 + 8 * int(cu[-1]) for (_, cu, _, _) in segs]
+        gbs = sum(app_bytes) / (sum(app_ms) * 1e-3) / 1e9
+        res["kv_append"] = {"kernel": "kv_append_kernel", "bound": "hbm", "avg_launch_ms": round(statistics.fmean(app_ms), 5),
+                            "bytes_per_launch": sum(app_bytes) / nchunks, "achieved": round(gbs, 1),
+                            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
     if w.n_requests == 1:
         res["per_chunk"]["schedule_model"] = schedule_report(med)
     if not args.no_gemm_ref:
