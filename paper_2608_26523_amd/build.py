@@ -28,14 +28,30 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(extra_flags=(), out: str = LIB, quiet: bool = True) -> str:
-    tmp = out + ".tmp"
-    cmd = [hipcc()] + HIPCC_FLAGS + list(extra_flags) + ["-I", INCLUDE, "-o", tmp, SRC]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    msgs = [ln for ln in (res.stdout + res.stderr).splitlines()
-            if "packed-fp32-ops" not in ln and ln.strip()]
-    if res.returncode != 0:
+PARTS = (0, 1)  # VPP_PART values: host code + contiguous-cache kernels, paged-cache kernels
+
+
+def build(extra_flags=(), out: str = LIB, quiet: bool = True, src: str = None) -> str:
+    """Compile the parts of the HIP source in parallel (one hipcc each), then link."""
+    src = src or SRC
+    base = [hipcc()] + HIPCC_FLAGS + list(extra_flags) + ["-I", INCLUDE]
+    objs = [out + ".part%d.o" % part for part in PARTS]
+    procs = []
+    for part, obj in zip(PARTS, objs):
+        cmd = [c for c in base if c != "-shared"] + ["-c", "-DVPP_PART=%d" % part, "-o", obj, src]
+        procs.append(subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True))
+    outs = [pr.communicate()[0] for pr in procs]
+    msgs = [ln for o in outs for ln in o.splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
+    if any(pr.returncode != 0 for pr in procs):
         raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
+    tmp = out + ".tmp"
+    res = subprocess.run(base + ["-o", tmp] + objs, capture_output=True, text=True)
+    msgs += [ln for ln in (res.stdout + res.stderr).splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
+    for obj in objs:
+        if os.path.exists(obj):
+            os.remove(obj)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc link failed:\n" + "\n".join(msgs))
     if msgs and not quiet:
         print("\n".join(msgs), file=sys.stderr)
     os.replace(tmp, out)

@@ -34,16 +34,22 @@
 
 #include "vpp_chunk_attn.h"
 
+// VPP_PART: 0 = host code and the contiguous-cache kernels, 1 = the paged-cache
+// kernels only; unset = everything in one translation unit.
+#ifndef VPP_PART
+#define VPP_PART 2
+#endif
+
 namespace {
 
 constexpr int BN = 64;         // keys per inner step
 constexpr int NWAVES = 4;
 // query rows per workgroup tile: 4 waves x NB blocks of 32 rows
 constexpr int block_rows(int nb) { return 32 * nb * NWAVES; }
-constexpr int BM_MAX = block_rows(2);
+[[maybe_unused]] constexpr int BM_MAX = block_rows(2);
 constexpr int NTHREADS = 64 * NWAVES;
 constexpr int MAX_SPLITS = 16;
-constexpr int STAGING_SLOTS = 4;
+[[maybe_unused]] constexpr int STAGING_SLOTS = 4;
 // Lazy rescale: the running max used for exp2 is refreshed only when a row's
 // max grows past it by more than this many powers of two; O and l share the
 // stale max, so the final quotient is unchanged and P stays <= 2^TAU.
@@ -99,6 +105,12 @@ __device__ __forceinline__ void copy16_to_lds(const i32x4& rsrc, uint32_t lds_ba
 typedef vpp_chunk_attn_work_item_t WorkItem;
 static_assert(sizeof(WorkItem) == 32, "work item layout");
 
+}  // namespace
+
+// Kernel argument blocks, shared by the translation units that instantiate
+// the kernels (the build compiles this file once per part, in parallel).
+namespace vpp_detail {
+
 struct AttnArgs {
     const WorkItem* items;
     const u16* q;
@@ -124,6 +136,28 @@ struct AttnArgs {
     int32_t page_shift;
     int32_t num_pages;   // page indices are clamped below it
 };
+
+// Arguments of the merge of split partials.
+struct CombineArgs {
+    const float* part_o;
+    const float* part_lse;
+    u16* out;
+    float* lse;
+    int64_t o_st, o_sh, lse_sh;
+    int32_t tokens, num_heads, splits;
+};
+
+hipError_t launch_attn_contig(int nb, int dqk, const AttnArgs& a, bool split, const CombineArgs& ca,
+                              hipStream_t stream);
+hipError_t launch_attn_paged(int nb, int dqk, const AttnArgs& a, bool split, const CombineArgs& ca,
+                             hipStream_t stream);
+
+}  // namespace vpp_detail
+
+namespace {
+
+using vpp_detail::AttnArgs;
+using vpp_detail::CombineArgs;
 
 // LDS tiles: K [BN][DQK] and V [BN][DV] bf16, row-major in 16-byte granules,
 // the granule index XOR-swizzled per row. The LDS serves 64 banks (256 bytes)
@@ -914,16 +948,8 @@ void attn_fwd_kernel(AttnArgs a) {
     }
 }
 
-// Merge of split partials: lse = log sum_s exp(lse_s); out = sum_s exp(lse_s - lse) O_s.
-struct CombineArgs {
-    const float* part_o;
-    const float* part_lse;
-    u16* out;
-    float* lse;
-    int64_t o_st, o_sh, lse_sh;
-    int32_t tokens, num_heads, splits;
-};
 
+// Merge of split partials: lse = log sum_s exp(lse_s); out = sum_s exp(lse_s - lse) O_s.
 template <int DV>
 __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
     constexpr int G = DV / 4;  // threads per (row, head): 4 values each
@@ -959,13 +985,56 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
     if (c == 0 && a.lse) a.lse[(int64_t)h * a.lse_sh + row] = mx + __logf(den);
 }
 
-size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+[[maybe_unused]] size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+template <int DQK, int DV, int NB, bool PAGED>
+hipError_t launch(const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
+    const int64_t total = (int64_t)a.num_items * a.num_heads;
+    if (total <= 0) return hipSuccess;
+    if (total > (int64_t)INT32_MAX) return hipErrorInvalidValue;
+    dim3 grid((unsigned)total), block(NTHREADS);
+    if (split) {
+        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, true, PAGED>), grid, block, 0, stream, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int64_t threads = (int64_t)ca.tokens * ca.num_heads * (DV / 4);
+        dim3 cg((unsigned)((threads + 255) / 256));
+        hipLaunchKernelGGL((combine_kernel<DV>), cg, dim3(256), 0, stream, ca);
+    } else {
+        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, false, PAGED>), grid, block, 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
+template <bool PAGED>
+hipError_t launch_dims(int nb, int dqk, const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
+    if (nb == 1) {
+        if (dqk == 64) return launch<64, 64, 1, PAGED>(a, split, ca, stream);
+        if (dqk == 128) return launch<128, 128, 1, PAGED>(a, split, ca, stream);
+        return launch<192, 128, 1, PAGED>(a, split, ca, stream);
+    }
+    if (dqk == 64) return launch<64, 64, 2, PAGED>(a, split, ca, stream);
+    if (dqk == 128) return launch<128, 128, 2, PAGED>(a, split, ca, stream);
+    return launch<192, 128, 2, PAGED>(a, split, ca, stream);
+}
 
 }  // namespace
 
-// ---------------------------------------------------------------------------
-// host side: plan
-// ---------------------------------------------------------------------------
+#if VPP_PART != 1
+hipError_t vpp_detail::launch_attn_contig(int nb, int dqk, const AttnArgs& a, bool split,
+                                          const CombineArgs& ca, hipStream_t stream) {
+    return launch_dims<false>(nb, dqk, a, split, ca, stream);
+}
+#endif
+#if VPP_PART != 0
+hipError_t vpp_detail::launch_attn_paged(int nb, int dqk, const AttnArgs& a, bool split,
+                                         const CombineArgs& ca, hipStream_t stream) {
+    return launch_dims<true>(nb, dqk, a, split, ca, stream);
+}
+#endif
+
+#if VPP_PART != 1
+
 // Scatter of a chunk's new K/V rows into a paged cache: the write that puts a
 // chunk's own keys and values in the cache before its attention (section 2.4).
 // One thread moves one 16-byte granule; consecutive threads walk the granules
@@ -1007,6 +1076,9 @@ __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// host side: plan
+// ---------------------------------------------------------------------------
 struct vpp_chunk_attn_plan_s {
     vpp_chunk_attn_config_t cfg;
     float scale;
@@ -1257,37 +1329,6 @@ namespace {
 bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 bool stride_ok(int64_t s) { return s > 0 && (s % 8) == 0; }
 
-template <int DQK, int DV, int NB, bool PAGED>
-hipError_t launch(const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
-    const int64_t total = (int64_t)a.num_items * a.num_heads;
-    if (total <= 0) return hipSuccess;
-    if (total > (int64_t)INT32_MAX) return hipErrorInvalidValue;
-    dim3 grid((unsigned)total), block(NTHREADS);
-    if (split) {
-        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, true, PAGED>), grid, block, 0, stream, a);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        const int64_t threads = (int64_t)ca.tokens * ca.num_heads * (DV / 4);
-        dim3 cg((unsigned)((threads + 255) / 256));
-        hipLaunchKernelGGL((combine_kernel<DV>), cg, dim3(256), 0, stream, ca);
-    } else {
-        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, false, PAGED>), grid, block, 0, stream, a);
-    }
-    return hipGetLastError();
-}
-
-template <bool PAGED>
-hipError_t launch_dims(int nb, int dqk, const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
-    if (nb == 1) {
-        if (dqk == 64) return launch<64, 64, 1, PAGED>(a, split, ca, stream);
-        if (dqk == 128) return launch<128, 128, 1, PAGED>(a, split, ca, stream);
-        return launch<192, 128, 1, PAGED>(a, split, ca, stream);
-    }
-    if (dqk == 64) return launch<64, 64, 2, PAGED>(a, split, ca, stream);
-    if (dqk == 128) return launch<128, 128, 2, PAGED>(a, split, ca, stream);
-    return launch<192, 128, 2, PAGED>(a, split, ca, stream);
-}
-
 int env_xcd_remap() {
     const char* s = getenv("VPP_XCD_REMAP");
     return s ? atoi(s) : 1;
@@ -1399,8 +1440,8 @@ vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int6
         ca.num_heads = c.num_q_heads;
         ca.splits = p->num_splits;
     }
-    const hipError_t e = pg ? launch_dims<true>(p->nb, c.head_dim_qk, a, split, ca, stream)
-                            : launch_dims<false>(p->nb, c.head_dim_qk, a, split, ca, stream);
+    const hipError_t e = pg ? vpp_detail::launch_attn_paged(p->nb, c.head_dim_qk, a, split, ca, stream)
+                            : vpp_detail::launch_attn_contig(p->nb, c.head_dim_qk, a, split, ca, stream);
     return e == hipSuccess ? VPP_OK : VPP_ERR_HIP;
 }
 
@@ -1502,3 +1543,5 @@ extern "C" vpp_status_t vpp_paged_slot_mapping(int32_t num_segments, const int32
     }
     return VPP_OK;
 }
+
+#endif  // VPP_PART != 1
