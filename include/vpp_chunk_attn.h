@@ -119,6 +119,30 @@ vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t plan,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Split key layout of the MLA models the paper evaluates (section 6.1: its
+ * DeepSeek model runs MLA attention, MHA-style in prefill): each key is the
+ * concatenation of a per-head part and a part shared by all heads,
+ *   K[j][h] = ( k_nope[j][h][0..127], k_rope[j][0..63] ),   dqk = 192, dv = 128,
+ * so the shared 64 dims are stored once per row instead of once per head (a
+ * third less key memory and traffic). Layouts (device memory, caller-owned):
+ *   k_nope bf16 [rows][Hkv][128]  strides kn_stride_tok, kn_stride_head
+ *   k_rope bf16 [rows][64]        stride kr_stride_tok
+ * Everything else (q with dqk = 192, v, out, lse, plan, workspace, stream) is
+ * as for vpp_chunk_attn_run, and so are the results: the same bits as
+ * vpp_chunk_attn_run over the concatenated keys. Errors: VPP_ERR_UNSUPPORTED
+ * unless the plan's head dims are (192, 128); VPP_ERR_INVALID_ARG for a null or
+ * misaligned k_rope or a bad kr_stride_tok; every error of vpp_chunk_attn_run.
+ */
+vpp_status_t vpp_chunk_attn_run_mla(vpp_chunk_attn_plan_t plan,
+                                    const void* q, int64_t q_stride_tok, int64_t q_stride_head,
+                                    const void* k_nope, int64_t kn_stride_tok, int64_t kn_stride_head,
+                                    const void* k_rope, int64_t kr_stride_tok,
+                                    const void* v_cache, int64_t v_stride_tok, int64_t v_stride_head,
+                                    void* out, int64_t o_stride_tok, int64_t o_stride_head,
+                                    float* lse, int64_t lse_stride_head,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Paged KV cache. The paper's system runs inside a serving engine (vLLM,
  * sections 5.4 and 6.1) whose KV cache is cut into fixed-size pages assigned
  * to requests through block tables; the chunk semantics are unchanged

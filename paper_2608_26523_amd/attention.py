@@ -2,8 +2,8 @@
 
 ``ChunkAttention`` validates tensors, owns a plan and a device workspace, and
 passes raw pointers and element strides to ``vpp_chunk_attn_plan`` /
-``vpp_chunk_attn_run`` (contiguous cache) or ``vpp_chunk_attn_run_paged`` (paged
-cache); ``kv_append_paged`` wraps ``vpp_kv_append_paged``. Nothing here does
+``vpp_chunk_attn_run`` (contiguous cache), ``vpp_chunk_attn_run_paged`` (paged
+cache) or ``vpp_chunk_attn_run_mla`` (keys split into per-head and shared parts); ``kv_append_paged`` wraps ``vpp_kv_append_paged``. Nothing here does
 arithmetic of its own.
 """
 from __future__ import annotations
@@ -128,6 +128,36 @@ class ChunkAttention:
                              out.data_ptr(), out.stride(0), out.stride(1),
                              lse_ptr, lse_sh,
                              self._ws.data_ptr(), self._ws.numel(), s.cuda_stream)
+        return out, lse
+
+    def run_mla(self, q: torch.Tensor, k_nope: torch.Tensor, k_rope: torch.Tensor, v_cache: torch.Tensor,
+                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                stream: Optional[torch.cuda.Stream] = None):
+        """Like ``run`` with the keys split as in the MLA models: k_nope [rows, Hkv, 128] per
+        head and k_rope [rows, 64] shared by all heads (head dims (192, 128) only)."""
+        out, lse_ptr, lse_sh = self._io(q, out, lse)
+        c = self.cfg
+        if c.head_dim_qk != 192 or c.head_dim_v != 128:
+            raise ValueError("the split key layout needs head dims (192, 128)")
+        self._check(k_nope, "k_nope", torch.bfloat16, 3)
+        self._check(k_rope, "k_rope", torch.bfloat16, 2)
+        self._check(v_cache, "v_cache", torch.bfloat16, 3)
+        if k_nope.shape[1] != c.num_kv_heads or k_nope.shape[2] != 128 or k_rope.shape[1] != 64:
+            raise ValueError("k_nope %s / k_rope %s do not match the config"
+                             % (tuple(k_nope.shape), tuple(k_rope.shape)))
+        if v_cache.shape[1] != c.num_kv_heads or v_cache.shape[2] != c.head_dim_v:
+            raise ValueError("v_cache shape %s does not match the config" % (tuple(v_cache.shape),))
+        if min(k_nope.shape[0], k_rope.shape[0], v_cache.shape[0]) < self.max_row:
+            raise ValueError("the planned chunk reads cache rows up to %d" % self.max_row)
+        s = stream if stream is not None else torch.cuda.current_stream(q.device)
+        B.vpp_chunk_attn_run_mla(self._plan,
+                                 q.data_ptr(), q.stride(0), q.stride(1),
+                                 k_nope.data_ptr(), k_nope.stride(0), k_nope.stride(1),
+                                 k_rope.data_ptr(), k_rope.stride(0),
+                                 v_cache.data_ptr(), v_cache.stride(0), v_cache.stride(1),
+                                 out.data_ptr(), out.stride(0), out.stride(1),
+                                 lse_ptr, lse_sh,
+                                 self._ws.data_ptr(), self._ws.numel(), s.cuda_stream)
         return out, lse
 
     def run_paged(self, q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,

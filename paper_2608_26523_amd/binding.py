@@ -25,6 +25,7 @@ EXPORTED = [
     "vpp_chunk_attn_plan", "vpp_chunk_attn_run", "vpp_chunk_attn_destroy",
     "vpp_status_str", "vpp_chunk_attn_plan_info", "vpp_chunk_attn_plan_items",
     "vpp_chunk_attn_run_paged", "vpp_kv_append_paged", "vpp_paged_slot_mapping",
+    "vpp_chunk_attn_run_mla",
 ]
 
 
@@ -97,6 +98,9 @@ def load(path: Optional[str] = None):
     lib.vpp_chunk_attn_run_paged.restype = ctypes.c_int
     lib.vpp_chunk_attn_run_paged.argtypes = [vp, vp, i64, i64, vp, i64, i64, i64, vp, i64, i64, i64,
                                              i32, i32, vp, i64, vp, i64, i64, vp, i64, vp, sz, vp]
+    lib.vpp_chunk_attn_run_mla.restype = ctypes.c_int
+    lib.vpp_chunk_attn_run_mla.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, i64, vp, i64, i64,
+                                           vp, i64, i64, vp, i64, vp, sz, vp]
     lib.vpp_kv_append_paged.restype = ctypes.c_int
     lib.vpp_kv_append_paged.argtypes = [vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, vp, i64, i64, i64,
                                         i32, i32, i32, i32, i32, i32, vp, vp]
@@ -157,6 +161,17 @@ def vpp_chunk_attn_run_paged(plan: int, q_ptr: int, q_st: int, q_sh: int, k_ptr:
                                          stream)
     if st != VPP_OK:
         raise VppError(st, "vpp_chunk_attn_run_paged")
+
+
+def vpp_chunk_attn_run_mla(plan: int, q_ptr: int, q_st: int, q_sh: int, kn_ptr: int, kn_st: int,
+                           kn_sh: int, kr_ptr: int, kr_st: int, v_ptr: int, v_st: int, v_sh: int,
+                           out_ptr: int, o_st: int, o_sh: int, lse_ptr: int, lse_sh: int, ws_ptr: int,
+                           ws_bytes: int, stream: int) -> None:
+    st = load().vpp_chunk_attn_run_mla(plan, q_ptr, q_st, q_sh, kn_ptr, kn_st, kn_sh, kr_ptr, kr_st,
+                                       v_ptr, v_st, v_sh, out_ptr, o_st, o_sh, lse_ptr, lse_sh,
+                                       ws_ptr, ws_bytes, stream)
+    if st != VPP_OK:
+        raise VppError(st, "vpp_chunk_attn_run_mla")
 
 
 def vpp_kv_append_paged(kn_ptr: int, kn_st: int, kn_sh: int, vn_ptr: int, vn_st: int, vn_sh: int,

@@ -28,7 +28,7 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-PARTS = (0, 1)  # VPP_PART values: host code + contiguous-cache kernels, paged-cache kernels
+PARTS = (0, 1, 2)  # VPP_PART values: host code + contiguous-cache kernels, paged, split-key
 
 
 def build(extra_flags=(), out: str = LIB, quiet: bool = True, src: str = None) -> str:

@@ -35,9 +35,10 @@
 #include "vpp_chunk_attn.h"
 
 // VPP_PART: 0 = host code and the contiguous-cache kernels, 1 = the paged-cache
-// kernels only; unset = everything in one translation unit.
+// kernels, 2 = the split-key-layout kernels; unset (3) = everything in one
+// translation unit.
 #ifndef VPP_PART
-#define VPP_PART 2
+#define VPP_PART 3
 #endif
 
 namespace {
@@ -50,6 +51,10 @@ constexpr int block_rows(int nb) { return 32 * nb * NWAVES; }
 constexpr int NTHREADS = 64 * NWAVES;
 constexpr int MAX_SPLITS = 16;
 [[maybe_unused]] constexpr int STAGING_SLOTS = 4;
+// cache layouts (kernel template argument KVM)
+constexpr int KV_CONTIG = 0, KV_PAGED = 1, KV_ROPE = 2;
+// split key layout: granules of the per-head and of the shared part of a K row
+constexpr int NOPE_GR = 16, ROPE_GR = 8;
 // Lazy rescale: the running max used for exp2 is refreshed only when a row's
 // max grows past it by more than this many powers of two; O and l share the
 // stale max, so the final quotient is unchanged and P stays <= 2^TAU.
@@ -135,6 +140,10 @@ struct AttnArgs {
     int64_t k_sp, v_sp;  // element strides between pages
     int32_t page_shift;
     int32_t num_pages;   // page indices are clamped below it
+    // Split key layout (KV_ROPE kernels only): k holds the per-head 128 dims of
+    // each key, k_rope [rows][64] the 64 dims shared by all heads.
+    const u16* k_rope;
+    int32_t kr_st;
 };
 
 // Arguments of the merge of split partials.
@@ -151,6 +160,7 @@ hipError_t launch_attn_contig(int nb, int dqk, const AttnArgs& a, bool split, co
                               hipStream_t stream);
 hipError_t launch_attn_paged(int nb, int dqk, const AttnArgs& a, bool split, const CombineArgs& ca,
                              hipStream_t stream);
+hipError_t launch_attn_rope(int nb, const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream);
 
 }  // namespace vpp_detail
 
@@ -471,9 +481,16 @@ __device__ __forceinline__ void static_range(F&& f) {
 // NB = 2: 64 query rows per wave, one workgroup (4 waves) per CU. NB = 1: 32
 // rows per wave and half the registers, so two workgroups share a CU and each
 // SIMD interleaves two waves' instruction streams.
-template <int DQK, int DV, int NB, bool SPLIT, bool PAGED>
+// KVM: the cache layout. KV_CONTIG: K [rows][Hkv][dqk] and V [rows][Hkv][dv];
+// KV_PAGED: the same rows in pages reached through a block table; KV_ROPE
+// (dqk = 192 only): K split into a per-head part k_nope [rows][Hkv][128] and a
+// part shared by all heads k_rope [rows][64], the key layout of the MLA models.
+template <int DQK, int DV, int NB, bool SPLIT, int KVM>
 __global__ __attribute__((amdgpu_flat_work_group_size(NTHREADS, NTHREADS), amdgpu_waves_per_eu(3 - NB, 3 - NB)))
 void attn_fwd_kernel(AttnArgs a) {
+    constexpr bool PAGED = KVM == KV_PAGED;
+    constexpr bool ROPE = KVM == KV_ROPE;
+    static_assert(!ROPE || DQK == 192, "the split key layout is 128 + 64 dims");
     typedef Tiles<DQK, DV, NB> T;
     typedef Atoms<NB> A;
     constexpr int KS = T::KS;
@@ -553,12 +570,30 @@ void attn_fwd_kernel(AttnArgs a) {
     // tile's first key row and whose size ends at the last key of the range:
     // rows past the range read as zeros (buffer range check), so the last tile
     // needs no special case. Per-lane byte offsets are fixed for the kernel.
+    // Split key layout: the K tile is two LDS regions, the per-head part
+    // [BN][NOPE_GR] granules then the shared part [BN][ROPE_GR], each filled by
+    // its own copies (a copy instruction has one source) and swizzled for its
+    // own row width; the first NOPE_LOADS copies read k_nope, the rest k_rope.
+    constexpr int NOPE_LOADS = BN * NOPE_GR / NTHREADS;
+    constexpr int NOPE_BYTES = BN * NOPE_GR * 16;
     uint32_t k_src[T::K_LOADS], v_src[T::V_LOADS];
 #pragma unroll
     for (int t = 0; t < T::K_LOADS; ++t) {
-        const int slot = t * NTHREADS + tid;
-        const int row = slot / T::KGR, gs = slot % T::KGR;
-        k_src[t] = (uint32_t)(row * (int)a.k_st + kswz<T::KGR>(row, gs) * 8) * 2u;
+        if constexpr (ROPE) {
+            if (t < NOPE_LOADS) {
+                const int slot = t * NTHREADS + tid;
+                const int row = slot / NOPE_GR, gs = slot % NOPE_GR;
+                k_src[t] = (uint32_t)(row * (int)a.k_st + kswz<NOPE_GR>(row, gs) * 8) * 2u;
+            } else {
+                const int slot = (t - NOPE_LOADS) * NTHREADS + tid;
+                const int row = slot / ROPE_GR, gs = slot % ROPE_GR;
+                k_src[t] = (uint32_t)(row * (int)a.kr_st + kswz<ROPE_GR>(row, gs) * 8) * 2u;
+            }
+        } else {
+            const int slot = t * NTHREADS + tid;
+            const int row = slot / T::KGR, gs = slot % T::KGR;
+            k_src[t] = (uint32_t)(row * (int)a.k_st + kswz<T::KGR>(row, gs) * 8) * 2u;
+        }
     }
 #pragma unroll
     for (int t = 0; t < T::V_LOADS; ++t) {
@@ -570,14 +605,25 @@ void attn_fwd_kernel(AttnArgs a) {
     auto k_rsrc = [&](int kt) {
         return make_rsrc(tile_src(kbase, a.k_sp, a.k_st, kt), max(0, min(BN, ke - kt)) * (int)a.k_st * 2);
     };
+    // the shared key part of the same rows (split layout; one row per key, no head)
+    const u16* rbase = ROPE ? a.k_rope + cache_row0 * a.kr_st : nullptr;
+    auto kr_rsrc = [&](int kt) {
+        return make_rsrc(rbase + (int64_t)kt * a.kr_st, max(0, min(BN, ke - kt)) * (int)a.kr_st * 2);
+    };
     auto v_rsrc = [&](int kt) {
         return make_rsrc(tile_src(vbase, a.v_sp, a.v_st, kt), max(0, min(BN, ke - kt)) * (int)a.v_st * 2);
     };
     const uint32_t lds_wave = (uint32_t)(uintptr_t)(lds_void_t*)smem + (uint32_t)wave * 1024u;
     // copy t of the K (V) tile into buffer B: LDS offset from this wave's base
-    auto load_k = [&](const i32x4& r, auto B, auto TT) {
-        constexpr int off = decltype(B)::value * T::K_BYTES + decltype(TT)::value * NWAVES * 1024;
-        copy16_to_lds<off>(r, lds_wave, k_src[decltype(TT)::value]);
+    auto load_k = [&](const i32x4& r, const i32x4& rr, auto B, auto TT) {
+        constexpr int t = decltype(TT)::value;
+        if constexpr (ROPE && t >= NOPE_LOADS) {
+            constexpr int off = decltype(B)::value * T::K_BYTES + NOPE_BYTES + (t - NOPE_LOADS) * NWAVES * 1024;
+            copy16_to_lds<off>(rr, lds_wave, k_src[t]);
+        } else {
+            constexpr int off = decltype(B)::value * T::K_BYTES + t * NWAVES * 1024;
+            copy16_to_lds<off>(r, lds_wave, k_src[t]);
+        }
     };
     auto load_v = [&](const i32x4& r, auto B, auto TT) {
         constexpr int off = 2 * T::K_BYTES + decltype(B)::value * T::V_BYTES + decltype(TT)::value * NWAVES * 1024;
@@ -585,7 +631,8 @@ void attn_fwd_kernel(AttnArgs a) {
     };
     auto issue_k = [&](auto B, int kt) {
         const i32x4 r = k_rsrc(kt);
-        static_for<T::K_LOADS>([&](auto TT) { load_k(r, B, TT); });
+        const i32x4 rr = ROPE ? kr_rsrc(kt) : r;
+        static_for<T::K_LOADS>([&](auto TT) { load_k(r, rr, B, TT); });
     };
     auto issue_v = [&](auto B, int kt) {
         const i32x4 r = v_rsrc(kt);
@@ -602,10 +649,18 @@ void attn_fwd_kernel(AttnArgs a) {
     // (row >> 1) & 7 depend only on lr. The swizzle touches the low 4 (or 3)
     // bits of the granule index, so K_OFFS offsets cover every ks and the
     // higher granule bits are an immediate.
-    constexpr int K_OFFS = (T::KGR % 16 == 0) ? 8 : 4;
-    int k_off[K_OFFS];
+    // (split key layout: K_OFFS offsets for the per-head region, KR_OFFS for the
+    // shared one)
+    constexpr int K_OFFS = ROPE ? NOPE_GR / 2 : ((T::KGR % 16 == 0) ? 8 : 4);
+    constexpr int KR_OFFS = ROPE ? ROPE_GR / 2 : 1;
+    int k_off[K_OFFS], kr_off[KR_OFFS];
 #pragma unroll
-    for (int r = 0; r < K_OFFS; ++r) k_off[r] = lr * (T::KGR * 16) + kswz<T::KGR>(lr, r * 2 + lg) * 16;
+    for (int r = 0; r < K_OFFS; ++r) {
+        if constexpr (ROPE) k_off[r] = lr * (NOPE_GR * 16) + kswz<NOPE_GR>(lr, r * 2 + lg) * 16;
+        else k_off[r] = lr * (T::KGR * 16) + kswz<T::KGR>(lr, r * 2 + lg) * 16;
+    }
+#pragma unroll
+    for (int r = 0; r < KR_OFFS; ++r) kr_off[r] = ROPE ? lr * (ROPE_GR * 16) + kswz<ROPE_GR>(lr, r * 2 + lg) * 16 : 0;
     // V^T (A operand of O^T) through ds_read_b64_tr_b16: 16-lane group q reads
     // keys 4*(q>>1) + (j>>2) and value columns 16*(q&1) + 4*(j&3) .. +3, i.e.
     // granule 4*d + (tr_col >> 3) of value block d; key & 3 = tr_key & 3.
@@ -633,9 +688,16 @@ void attn_fwd_kernel(AttnArgs a) {
             for (int i = 0; i < 16; ++i) o[d][nb][i] = 0.f;
 
     auto load_kfrag = [&](const char* kt_buf, int ks, int mb) -> bf16x8 {
-        const u32x4 raw = *(const u32x4*)(kt_buf + mb * 32 * T::KGR * 16 + (ks / K_OFFS) * (K_OFFS * 32) +
-                                          k_off[ks % K_OFFS]);
-        return __builtin_bit_cast(bf16x8, raw);
+        if constexpr (ROPE) {
+            const char* addr = ks < NOPE_GR / 2
+                                   ? kt_buf + mb * 32 * NOPE_GR * 16 + k_off[ks]
+                                   : kt_buf + NOPE_BYTES + mb * 32 * ROPE_GR * 16 + kr_off[ks - NOPE_GR / 2];
+            return __builtin_bit_cast(bf16x8, *(const u32x4*)addr);
+        } else {
+            const u32x4 raw = *(const u32x4*)(kt_buf + mb * 32 * T::KGR * 16 + (ks / K_OFFS) * (K_OFFS * 32) +
+                                              k_off[ks % K_OFFS]);
+            return __builtin_bit_cast(bf16x8, raw);
+        }
     };
     auto load_vfrag = [&](const char* vt, int mb, int hh, int d) -> bf16x8 {
         bf16x8 af;
@@ -672,6 +734,9 @@ void attn_fwd_kernel(AttnArgs a) {
     uint64_t k_next = PAGED ? 0 : (uint64_t)(uintptr_t)(kbase + (int64_t)(kb + 2 * BN) * a.k_st);
     uint64_t v_next = PAGED ? 0 : (uint64_t)(uintptr_t)(vbase + (int64_t)(kb + BN) * a.v_st);
     int k_rows = ke - kb - 2 * BN, v_rows = ke - kb - BN;
+    // split key layout: the shared part's running source (same rows as K)
+    const int kr_row_bytes = ROPE ? (int)a.kr_st * 2 : 0;
+    uint64_t kr_next = ROPE ? (uint64_t)(uintptr_t)(rbase + (int64_t)(kb + 2 * BN) * a.kr_st) : 0;
     // paged cache: the page of the K tile a step copies is read one step ahead
     // (raw, clamped at its use), and V(t+1) shares K(t+1)'s page
     int pg_pending = 0, pg_prev = 0;
@@ -713,6 +778,11 @@ void attn_fwd_kernel(AttnArgs a) {
         const int v_bytes = v_rows >= BN ? BN * v_row_bytes : (v_rows > 0 ? v_rows * v_row_bytes : 0);
         const i32x4 rk = make_rsrc((const void*)k_next, k_bytes);
         const i32x4 rv = make_rsrc((const void*)v_next, v_bytes);
+        i32x4 rkr = rk;
+        if constexpr (ROPE) {
+            rkr = make_rsrc((const void*)kr_next, k_rows >= BN ? BN * kr_row_bytes : (k_rows > 0 ? k_rows * kr_row_bytes : 0));
+            kr_next += BN * kr_row_bytes;
+        }
         if constexpr (!PAGED) {
             k_next += BN * k_row_bytes;
             v_next += BN * v_row_bytes;
@@ -839,7 +909,8 @@ void attn_fwd_kernel(AttnArgs a) {
                         if constexpr (j < T::V_LOADS) {
                             load_v(rv, std::integral_constant<int, 1 - par>(), std::integral_constant<int, j>());
                         } else {
-                            load_k(rk, std::integral_constant<int, par>(), std::integral_constant<int, j - T::V_LOADS>());
+                            load_k(rk, rkr, std::integral_constant<int, par>(),
+                                   std::integral_constant<int, j - T::V_LOADS>());
                         }
                     }
                 }
@@ -987,53 +1058,65 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
 
 [[maybe_unused]] size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-template <int DQK, int DV, int NB, bool PAGED>
+template <int DQK, int DV, int NB, int KVM>
 hipError_t launch(const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
     const int64_t total = (int64_t)a.num_items * a.num_heads;
     if (total <= 0) return hipSuccess;
     if (total > (int64_t)INT32_MAX) return hipErrorInvalidValue;
     dim3 grid((unsigned)total), block(NTHREADS);
     if (split) {
-        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, true, PAGED>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, true, KVM>), grid, block, 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int64_t threads = (int64_t)ca.tokens * ca.num_heads * (DV / 4);
         dim3 cg((unsigned)((threads + 255) / 256));
         hipLaunchKernelGGL((combine_kernel<DV>), cg, dim3(256), 0, stream, ca);
     } else {
-        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, false, PAGED>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((attn_fwd_kernel<DQK, DV, NB, false, KVM>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
 }
 
-template <bool PAGED>
+template <int KVM>
 hipError_t launch_dims(int nb, int dqk, const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
-    if (nb == 1) {
-        if (dqk == 64) return launch<64, 64, 1, PAGED>(a, split, ca, stream);
-        if (dqk == 128) return launch<128, 128, 1, PAGED>(a, split, ca, stream);
-        return launch<192, 128, 1, PAGED>(a, split, ca, stream);
+    if constexpr (KVM == KV_ROPE) {
+        // the split key layout exists for dqk = 192 only (the caller checks)
+        if (nb == 1) return launch<192, 128, 1, KVM>(a, split, ca, stream);
+        return launch<192, 128, 2, KVM>(a, split, ca, stream);
+    } else {
+        if (nb == 1) {
+            if (dqk == 64) return launch<64, 64, 1, KVM>(a, split, ca, stream);
+            if (dqk == 128) return launch<128, 128, 1, KVM>(a, split, ca, stream);
+            return launch<192, 128, 1, KVM>(a, split, ca, stream);
+        }
+        if (dqk == 64) return launch<64, 64, 2, KVM>(a, split, ca, stream);
+        if (dqk == 128) return launch<128, 128, 2, KVM>(a, split, ca, stream);
+        return launch<192, 128, 2, KVM>(a, split, ca, stream);
     }
-    if (dqk == 64) return launch<64, 64, 2, PAGED>(a, split, ca, stream);
-    if (dqk == 128) return launch<128, 128, 2, PAGED>(a, split, ca, stream);
-    return launch<192, 128, 2, PAGED>(a, split, ca, stream);
 }
 
 }  // namespace
 
-#if VPP_PART != 1
+#if VPP_PART == 0 || VPP_PART == 3
 hipError_t vpp_detail::launch_attn_contig(int nb, int dqk, const AttnArgs& a, bool split,
                                           const CombineArgs& ca, hipStream_t stream) {
-    return launch_dims<false>(nb, dqk, a, split, ca, stream);
+    return launch_dims<KV_CONTIG>(nb, dqk, a, split, ca, stream);
 }
 #endif
-#if VPP_PART != 0
+#if VPP_PART == 1 || VPP_PART == 3
 hipError_t vpp_detail::launch_attn_paged(int nb, int dqk, const AttnArgs& a, bool split,
                                          const CombineArgs& ca, hipStream_t stream) {
-    return launch_dims<true>(nb, dqk, a, split, ca, stream);
+    return launch_dims<KV_PAGED>(nb, dqk, a, split, ca, stream);
+}
+#endif
+#if VPP_PART == 2 || VPP_PART == 3
+hipError_t vpp_detail::launch_attn_rope(int nb, const AttnArgs& a, bool split, const CombineArgs& ca,
+                                        hipStream_t stream) {
+    return launch_dims<KV_ROPE>(nb, 192, a, split, ca, stream);
 }
 #endif
 
-#if VPP_PART != 1
+#if VPP_PART == 0 || VPP_PART == 3
 
 // Scatter of a chunk's new K/V rows into a paged cache: the write that puts a
 // chunk's own keys and values in the cache before its attention (section 2.4).
@@ -1345,10 +1428,16 @@ struct PagedKV {
     int32_t page_shift, num_pages;
 };
 
+// Shared key part of the split key layout (see vpp_chunk_attn_run_mla).
+struct RopeK {
+    const void* k_rope;
+    int64_t kr_st;
+};
+
 vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int64_t q_sh, const void* k,
                       int64_t k_st, int64_t k_sh, const void* v, int64_t v_st, int64_t v_sh, void* out,
                       int64_t o_st, int64_t o_sh, float* lse, int64_t lse_sh, void* workspace,
-                      size_t workspace_bytes, void* stream_ptr, const PagedKV* pg) {
+                      size_t workspace_bytes, void* stream_ptr, const PagedKV* pg, const RopeK* rope = nullptr) {
     if (!p) return VPP_ERR_INVALID_ARG;
     if (!q || !k || !v || !out) return VPP_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return VPP_ERR_INVALID_ARG;
@@ -1362,6 +1451,12 @@ vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int6
     if (q_st >= smax || q_sh >= smax || k_st >= smax || k_sh >= smax || v_st >= smax || v_sh >= smax ||
         o_st >= smax || o_sh >= smax || (lse && lse_sh >= ((int64_t)1 << 31)))
         return VPP_ERR_INVALID_ARG;
+    if (rope) {
+        if (p->cfg.head_dim_qk != 192 || p->cfg.head_dim_v != 128) return VPP_ERR_UNSUPPORTED;
+        if (!rope->k_rope || !aligned16(rope->k_rope) || !stride_ok(rope->kr_st) || rope->kr_st < 64 ||
+            rope->kr_st >= smax)
+            return VPP_ERR_INVALID_ARG;
+    }
     if (!workspace || ((uintptr_t)workspace & 255u) != 0) return VPP_ERR_WORKSPACE;
     if (workspace_bytes < p->ws_bytes) return VPP_ERR_WORKSPACE;
     if (p->items.empty()) return VPP_OK;  // nothing to do: every segment is empty
@@ -1415,6 +1510,10 @@ vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int6
     a.tokens = p->tokens;
     a.scale_log2 = (float)((double)p->scale * 1.4426950408889634);
     a.xcd_remap = env_xcd_remap();
+    if (rope) {
+        a.k_rope = (const u16*)rope->k_rope;
+        a.kr_st = (int32_t)rope->kr_st;
+    }
     if (pg) {
         a.block_table = pg->block_table;
         a.bt_st = pg->bt_st;
@@ -1440,8 +1539,9 @@ vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int6
         ca.num_heads = c.num_q_heads;
         ca.splits = p->num_splits;
     }
-    const hipError_t e = pg ? vpp_detail::launch_attn_paged(p->nb, c.head_dim_qk, a, split, ca, stream)
-                            : vpp_detail::launch_attn_contig(p->nb, c.head_dim_qk, a, split, ca, stream);
+    const hipError_t e = rope ? vpp_detail::launch_attn_rope(p->nb, a, split, ca, stream)
+                         : pg ? vpp_detail::launch_attn_paged(p->nb, c.head_dim_qk, a, split, ca, stream)
+                              : vpp_detail::launch_attn_contig(p->nb, c.head_dim_qk, a, split, ca, stream);
     return e == hipSuccess ? VPP_OK : VPP_ERR_HIP;
 }
 
@@ -1454,6 +1554,17 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
                                            void* stream_ptr) {
     return run_impl(p, q, q_st, q_sh, k, k_st, k_sh, v, v_st, v_sh, out, o_st, o_sh, lse, lse_sh, workspace,
                     workspace_bytes, stream_ptr, nullptr);
+}
+
+extern "C" vpp_status_t vpp_chunk_attn_run_mla(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st,
+                                               int64_t q_sh, const void* k_nope, int64_t kn_st, int64_t kn_sh,
+                                               const void* k_rope, int64_t kr_st, const void* v, int64_t v_st,
+                                               int64_t v_sh, void* out, int64_t o_st, int64_t o_sh, float* lse,
+                                               int64_t lse_sh, void* workspace, size_t workspace_bytes,
+                                               void* stream_ptr) {
+    RopeK rope{k_rope, kr_st};
+    return run_impl(p, q, q_st, q_sh, k_nope, kn_st, kn_sh, v, v_st, v_sh, out, o_st, o_sh, lse, lse_sh,
+                    workspace, workspace_bytes, stream_ptr, nullptr, &rope);
 }
 
 extern "C" vpp_status_t vpp_chunk_attn_run_paged(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st,
@@ -1544,4 +1655,4 @@ extern "C" vpp_status_t vpp_paged_slot_mapping(int32_t num_segments, const int32
     return VPP_OK;
 }
 
-#endif  // VPP_PART != 1
+#endif  // host code (part 0)

@@ -76,3 +76,22 @@ def test_kv_append_no_tokens_is_a_no_op():
     st = B.load().vpp_kv_append_paged(0, 256, 128, 0, 256, 128, 0, 16384, 256, 128,
                                       0, 16384, 256, 128, 0, 2, 128, 128, 64, 4, 0, None)
     assert st == B.VPP_OK
+
+
+def test_run_mla_rejects():
+    lib = B.load()
+    h, ws = B.vpp_chunk_attn_plan(_cfg(), [0, 100], [0], [50])        # (128, 128): no split keys
+    try:
+        st = lib.vpp_chunk_attn_run_mla(h, FAKE, 512, 128, FAKE, 512, 128, FAKE, 64, FAKE, 512, 128,
+                                        FAKE, 512, 128, None, 0, FAKE, ws, None)
+        assert st == B.VPP_ERR_UNSUPPORTED
+    finally:
+        B.vpp_chunk_attn_destroy(h)
+    h, ws = B.vpp_chunk_attn_plan(_cfg(hq=2, hkv=2, dqk=192, dv=128), [0, 100], [0], [50])
+    try:
+        for kr, kr_st in ((0, 64), (FAKE + 8, 64), (FAKE, 60), (FAKE, 0)):
+            st = lib.vpp_chunk_attn_run_mla(h, FAKE, 384, 192, FAKE, 256, 128, kr, kr_st, FAKE, 256, 128,
+                                            FAKE, 256, 128, None, 0, FAKE, ws, None)
+            assert st == B.VPP_ERR_INVALID_ARG, (kr, kr_st)
+    finally:
+        B.vpp_chunk_attn_destroy(h)
