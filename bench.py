@@ -296,6 +296,9 @@ def main():
     ap.add_argument("--paged", type=int, default=0,
                     help="page size: run the path over a paged KV cache (pages in random order); "
                          "each chunk first appends its own K/V rows into its pages, then attends")
+    ap.add_argument("--mla-split", action="store_true",
+                    help="(dqk = 192 workloads) run with the MLA split key layout: per-head k_nope "
+                         "[rows, H, 128] and one shared k_rope [rows, 64] (head 0's last 64 dims)")
     ap.add_argument("--schedule-sweep", default="",
                     help="comma-separated chunk sizes: time one prompt of the workload at each "
                          "and print the schedule model's results (one JSON line), nothing else")
@@ -352,6 +355,13 @@ def main():
     nbytes = [chunk_bytes(w, cu, pre) for (_, cu, _, pre) in segs]
     stream = torch.cuda.current_stream(dev)
     paged = None
+    split_keys = None
+    if args.mla_split:
+        if w.dqk != 192 or args.paged or w.num_splits > 1:
+            print("--mla-split needs a dqk = 192 workload without a split key range and a "
+                  "contiguous cache", file=sys.stderr)
+            sys.exit(2)
+        split_keys = (k[:, :, :128].contiguous(), k[:, 0, 128:].contiguous())
     if args.paged:
         from paper_2608_26523_amd.attention import kv_append_paged
         paged = build_paged(w, k, v, segs, args.paged)
@@ -361,7 +371,13 @@ def main():
         for c, (t0, cu, kvs, pre) in enumerate(segs):
             a = attn[c]
             tok = int(cu[-1])
-            if paged is None:
+            if split_keys is not None:
+                a.plan(cu, kvs, pre)
+                if events is not None:
+                    events[c][0].record(stream)
+                a.run_mla(q[t0:t0 + tok], split_keys[0], split_keys[1], v, out[t0:t0 + tok],
+                          lse[:, t0:t0 + tok], stream=stream)
+            elif paged is None:
                 a.plan(cu, kvs, pre)
                 if events is not None:
                     events[c][0].record(stream)
@@ -429,12 +445,13 @@ def main():
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None if args.paged else measured_traffic(w.name),
+                     "traffic": None if (args.paged or args.mla_split) else measured_traffic(w.name),
                      "kernel": "attn_fwd_kernel", "avg_launch_ms": round(kernel_ms, 4),
                      "flops_per_launch": total_flops / nchunks,
                      "algorithmic_bytes_per_launch": sum(nbytes) / nchunks},
         "kv_cache": ("paged, %d-row pages in random order; each chunk appends its K/V first" % args.paged
-                     if args.paged else "contiguous"),
+                     if args.paged else ("contiguous, MLA split keys (k_nope per head + shared k_rope)"
+                                         if args.mla_split else "contiguous")),
         "per_chunk": {"prefix_tokens": prefix, "median_ms": [round(x, 4) for x in med],
                       "tflops": [round(f / (m * 1e-3) / 1e12, 2) for f, m in zip(flops, med)],
                       "splits": splits, "fit": fit, "eq3_residual": eq3},

@@ -26,7 +26,7 @@ def _rand(shape, std, seed):
     return (torch.randn(shape, generator=g, device=DEV) * std).to(torch.bfloat16)
 
 
-def _attn(hq, max_tok, max_kv, splits=-1):
+def _attn(hq, max_tok, max_kv, splits=1):
     from paper_2608_26523_amd.attention import ChunkAttention
     return ChunkAttention(hq, hq, 192, 128, max_chunk_tokens=max_tok, max_kv_len=max_kv, num_splits=splits)
 
@@ -43,10 +43,14 @@ def _split_keys(rows, heads, seed):
 CASES = [
     (4, [(0, 0, 300)], 300, 1),
     (2, [(0, 130, 257)], 387, 1),
-    (4, [(0, 90, 300), (390, 0, 45), (435, 700, 170)], 1305, -1),
+    (4, [(0, 90, 300), (390, 0, 45), (435, 700, 170)], 1305, 1),
     (2, [(0, 1000, 131)], 1131, 3),
     (8, [(0, 4096, 256)], 4352, 4),
 ]
+
+
+SPLIT_OFF = ("split key ranges are switched off for the split key layout: a run with 4 splits "
+             "over a 524288-row cache faulted the GPU and its cause is not yet shown")
 
 
 @pytest.mark.parametrize("nb", [1, 2])
@@ -54,6 +58,8 @@ CASES = [
 def test_split_keys_equal_concatenated(case, nb, monkeypatch):
     monkeypatch.setenv("VPP_NB", str(nb))
     hq, segs, T, splits = CASES[case]
+    if splits > 1:
+        pytest.skip(SPLIT_OFF)
     print("case:", case, CASES[case], "nb", nb, flush=True)
     k_nope, k_rope, k_full = _split_keys(T, hq, 10 + case)
     v = _rand((T, hq, 128), 1.0 / math.sqrt(192), 20 + case)
@@ -93,6 +99,20 @@ def test_split_keys_vs_oracle():
     rep = PA.compare(out, lse, rows, heads, ro.reshape(tok * hq, -1), rl.T.reshape(-1))
     print(rep, flush=True)
     assert rep.ok(), str(rep)
+
+
+def test_split_keys_refuse_split_plans():
+    """The split key layout refuses plans with a split key range (switched off, see SPLIT_OFF)."""
+    from paper_2608_26523_amd import binding as B
+    hq, T = 2, 1131
+    k_nope, k_rope, _ = _split_keys(T, hq, 60)
+    v = _rand((T, hq, 128), 0.1, 61)
+    q = _rand((131, hq, 192), 0.1, 62)
+    attn = _attn(hq, 131, T, splits=3)
+    attn.plan([0, 131], [0], [1000])
+    with pytest.raises(B.VppError) as e:
+        attn.run_mla(q, k_nope, k_rope, v)
+    assert e.value.status == B.VPP_ERR_UNSUPPORTED
 
 
 def test_split_keys_full_size_mla_chunk():
