@@ -302,6 +302,8 @@ def main():
     ap.add_argument("--schedule-sweep", default="",
                     help="comma-separated chunk sizes: time one prompt of the workload at each "
                          "and print the schedule model's results (one JSON line), nothing else")
+    ap.add_argument("--gemm-ref-only", action="store_true",
+                    help="only run the library GEMM reference (a known kernel for counter passes)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB, three "
                          "times (the known-size kernel that scales the HBM byte counters)")
@@ -320,6 +322,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
+        return
+
+    if args.gemm_ref_only:
+        print(json.dumps(gemm_reference(torch.device("cuda", 0))), flush=True)
         return
 
     from paper_2608_26523_amd import workloads as W
@@ -397,7 +403,16 @@ def main():
             if events is not None:
                 events[c][1].record(stream)
 
-    for _ in range(warmup):
+    # the first pass over the chunks is timed on its own: the cold latency (plans built,
+    # caches cold); it is one of the warm-up steps when there are any
+    cold = None
+    if warmup > 0:
+        cold_ev = [[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+                   for _ in range(nchunks)]
+        step(cold_ev)
+        torch.cuda.synchronize()
+        cold = [cold_ev[c][0].elapsed_time(cold_ev[c][1]) for c in range(nchunks)]
+    for _ in range(max(0, warmup - 1)):
         step()
     torch.cuda.synchronize()
     ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
@@ -453,6 +468,8 @@ def main():
                      if args.paged else ("contiguous, MLA split keys (k_nope per head + shared k_rope)"
                                          if args.mla_split else "contiguous")),
         "per_chunk": {"prefix_tokens": prefix, "median_ms": [round(x, 4) for x in med],
+                      "min_ms": [round(min(x), 4) for x in per_chunk],
+                      "cold_ms": [round(x, 4) for x in cold] if cold else None,
                       "tflops": [round(f / (m * 1e-3) / 1e12, 2) for f, m in zip(flops, med)],
                       "splits": splits, "fit": fit, "eq3_residual": eq3},
     }
