@@ -204,9 +204,16 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
     return r;
 }
 
+// Plain v_max_f32: the scores are never NaN (masked ones are -inf), so the
+// canonicalising maxes fmaxf would add are not needed.
+__device__ __forceinline__ float max2f(float a, float b) {
+    float r;
+    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
 __device__ __forceinline__ float lane_swap32_max(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    return max2f(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float lane_swap32_add(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -814,13 +821,12 @@ void attn_fwd_kernel(AttnArgs a) {
             }
         }
 
-        float alpha[NB], m_use[NB], mx[NB], lsum[NB][2];
+        float alpha[NB], m_use[NB], mx[NB][4], lsum[NB][2];  // mx: one partial max per max atom
         bool refresh[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
             alpha[nb] = 1.f;
             m_use[nb] = 0.f;
-            mx[nb] = -INFINITY;
             lsum[nb][0] = lsum[nb][1] = 0.f;
             refresh[nb] = false;
         }
@@ -832,16 +838,21 @@ void attn_fwd_kernel(AttnArgs a) {
         auto atom = [&](auto K) {
             constexpr int k = decltype(K)::value;
             if constexpr (k < A::MAXF) {
-                // 4 max3 steps over 8 of the 32 scores of query block nb
+                // max of 8 of the 32 scores of query block nb, as a depth-2 tree:
+                // the four atoms of a row are independent of each other
                 constexpr int nb = k >> 2, q = k & 3;
-#pragma unroll
-                for (int j = 0; j < 8; j += 2) {
+                auto sc = [&](int j) -> float {
                     const int v = q * 8 + j;  // score index in [mb*16 + i]
-                    mx[nb] = max3f(mx[nb], s_cur[v >> 4][nb][v & 15], s_cur[(v + 1) >> 4][nb][(v + 1) & 15]);
-                }
+                    return s_cur[v >> 4][nb][v & 15];
+                };
+                const float t0 = max3f(sc(0), sc(1), sc(2));
+                const float t1 = max3f(sc(3), sc(4), sc(5));
+                const float t2 = max2f(sc(6), sc(7));
+                mx[nb][q] = max3f(t0, t1, t2);
             } else if constexpr (k < A::EXP) {
                 constexpr int nb = k - A::MAXF;
-                const float m = lane_swap32_max(mx[nb]) * a.scale_log2;
+                const float m =
+                    lane_swap32_max(max3f(mx[nb][0], mx[nb][1], max2f(mx[nb][2], mx[nb][3]))) * a.scale_log2;
                 // per-lane decision: the exps of this row wait only for VALU work;
                 // the wave-wide vote happens once, at the rescale check
                 refresh[nb] = m > m_run[nb] + LAZY_TAU;
