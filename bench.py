@@ -34,8 +34,10 @@ sys.path.insert(0, ROOT)
 METRIC = "chunked-prefill attention TFLOP/s (% bf16 MFMA peak) + per-chunk latency vs prefix"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
-DEFAULT_STEPS = {"tiny": 50, "gqa": 50, "mla": 5, "long": 2, "mixed": 2}
-DEFAULT_WARMUP = {"tiny": 5, "gqa": 5, "mla": 1, "long": 1, "mixed": 1}
+# per-chunk statistics want >= 20 timed runs; the long and mixed prompts take ~9 s and ~5 s
+# per step, so they stop at about a minute of timed work
+DEFAULT_STEPS = {"tiny": 50, "gqa": 50, "mla": 20, "long": 6, "mixed": 10}
+DEFAULT_WARMUP = {"tiny": 5, "gqa": 5, "mla": 3, "long": 1, "mixed": 1}
 
 
 def chunk_flops(w, cu, pre):
