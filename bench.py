@@ -237,6 +237,30 @@ def build_paged(w, k, v, segs, page, seed=0):
     return k_pages, v_pages, per_chunk
 
 
+MFMA_FILE = os.path.join(ROOT, "profiles", "attn_fwd_mfma_clock.md")
+
+
+def measured_mfma(workload):
+    """MFMA pipe utilisation (SQ_VALU_MFMA_BUSY_CYCLES over active cycles of all SIMDs) and the
+    shader clock of the attention kernel, from the committed counter summary; None unless it
+    was taken on the kernel source that is here now."""
+    import hashlib
+    try:
+        with open(KERNEL_SRC, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()[:16]
+        with open(MFMA_FILE) as f:
+            for ln in f:
+                parts = ln.split()
+                if len(parts) == 5 and parts[0] == "mfma" and parts[1] == workload and parts[2] == sha:
+                    busy, mhz = float(parts[3]), float(parts[4])
+                    return {"busy": busy, "clock_mhz": mhz,
+                            "busy_vs_peak_clock": round(busy * mhz / 2400.0, 4),
+                            "source": "rocprofv3 counters, profiles/attn_fwd_mfma_clock.md"}
+    except OSError:
+        return None
+    return None
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -463,6 +487,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": None if (args.paged or args.mla_split) else measured_traffic(w.name),
+                     "mfma_util": None if (args.paged or args.mla_split) else measured_mfma(w.name),
                      "kernel": "attn_fwd_kernel", "avg_launch_ms": round(kernel_ms, 4),
                      "flops_per_launch": total_flops / nchunks,
                      "algorithmic_bytes_per_launch": sum(nbytes) / nchunks},
