@@ -389,9 +389,8 @@ def main():
     paged = None
     split_keys = None
     if args.mla_split:
-        if w.dqk != 192 or args.paged or w.num_splits > 1:
-            print("--mla-split needs a dqk = 192 workload without a split key range and a "
-                  "contiguous cache", file=sys.stderr)
+        if w.dqk != 192 or args.paged:
+            print("--mla-split needs a dqk = 192 workload and a contiguous cache", file=sys.stderr)
             sys.exit(2)
         split_keys = (k[:, :, :128].contiguous(), k[:, 0, 128:].contiguous())
     if args.paged:

@@ -129,11 +129,10 @@ vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t plan,
  *   k_rope bf16 [rows][64]        stride kr_stride_tok
  * Everything else (q with dqk = 192, v, out, lse, plan, workspace, stream) is
  * as for vpp_chunk_attn_run, and so are the results: the same bits as
- * vpp_chunk_attn_run over the concatenated keys. Errors: VPP_ERR_UNSUPPORTED
- * unless the plan's head dims are (192, 128), and for plans that split the key
- * range (num_splits > 1: switched off for now); VPP_ERR_INVALID_ARG for a null
- * or misaligned k_rope or a bad kr_stride_tok (>= 64, a multiple of 8); every
- * error of vpp_chunk_attn_run.
+ * vpp_chunk_attn_run over the concatenated keys, split key ranges included.
+ * Errors: VPP_ERR_UNSUPPORTED unless the plan's head dims are (192, 128);
+ * VPP_ERR_INVALID_ARG for a null or misaligned k_rope or a bad kr_stride_tok
+ * (>= 64, a multiple of 8); every error of vpp_chunk_attn_run.
  */
 vpp_status_t vpp_chunk_attn_run_mla(vpp_chunk_attn_plan_t plan,
                                     const void* q, int64_t q_stride_tok, int64_t q_stride_head,

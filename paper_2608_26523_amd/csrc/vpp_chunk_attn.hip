@@ -100,11 +100,15 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, int32_t bytes) {
 // buffer they fill. Nothing else in the kernel keeps a value in M0.
 template <int OFF>
 __device__ __forceinline__ void copy16_to_lds(const i32x4& rsrc, uint32_t lds_base, uint32_t voff) {
-    // M0 = lds_base + OFF: one live SGPR for every copy of the kernel
+    // M0 = lds_base + OFF: one live SGPR for every copy of the kernel.
+    // The scalar add also writes SCC: without the clobber the compiler may
+    // place a copy between the two halves of a 64-bit scalar add and the high
+    // half then adds the copy's carry instead of its own (an address 4 GiB off
+    // whenever the low half wraps).
     asm volatile("s_add_u32 m0, %0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                  :
                  : "s"(lds_base), "v"(voff), "s"(rsrc), "i"(OFF)
-                 : "memory");
+                 : "memory", "scc");
 }
 
 typedef vpp_chunk_attn_work_item_t WorkItem;
@@ -1464,10 +1468,6 @@ vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int6
         return VPP_ERR_INVALID_ARG;
     if (rope) {
         if (p->cfg.head_dim_qk != 192 || p->cfg.head_dim_v != 128) return VPP_ERR_UNSUPPORTED;
-        // Switched off: a run of the split-key kernels with a split key range (a
-        // 524288-row cache, 4 splits) left the GPU faulted, and no cause has been
-        // shown yet; unsplit plans are unaffected.
-        if (p->num_splits > 1) return VPP_ERR_UNSUPPORTED;
         if (!rope->k_rope || !aligned16(rope->k_rope) || !stride_ok(rope->kr_st) || rope->kr_st < 64 ||
             rope->kr_st >= smax)
             return VPP_ERR_INVALID_ARG;

@@ -4,7 +4,10 @@ K[j][h] = (k_nope[j][h][0..127], k_rope[j][0..63]): the run over the split
 layout must give the same bits as the contiguous run over the concatenated keys
 (the kernels do the same arithmetic; only the LDS copy of K differs), for both
 tile variants, split and unsplit key ranges and multi-segment chunks, and at the
-mla workload's full size. One case is also checked against the fp64 oracle.
+full sizes of the mla workload and of the long workload (the latter with the
+split keys also given as views into the concatenated keys, whose row strides
+make every running copy address cross 4 GiB boundaries). One case is also
+checked against the fp64 oracle.
 """
 import math
 
@@ -49,17 +52,11 @@ CASES = [
 ]
 
 
-SPLIT_OFF = ("split key ranges are switched off for the split key layout: a run with 4 splits "
-             "over a 524288-row cache faulted the GPU and its cause is not yet shown")
-
-
 @pytest.mark.parametrize("nb", [1, 2])
 @pytest.mark.parametrize("case", range(len(CASES)))
 def test_split_keys_equal_concatenated(case, nb, monkeypatch):
     monkeypatch.setenv("VPP_NB", str(nb))
     hq, segs, T, splits = CASES[case]
-    if splits > 1:
-        pytest.skip(SPLIT_OFF)
     print("case:", case, CASES[case], "nb", nb, flush=True)
     k_nope, k_rope, k_full = _split_keys(T, hq, 10 + case)
     v = _rand((T, hq, 128), 1.0 / math.sqrt(192), 20 + case)
@@ -101,20 +98,6 @@ def test_split_keys_vs_oracle():
     assert rep.ok(), str(rep)
 
 
-def test_split_keys_refuse_split_plans():
-    """The split key layout refuses plans with a split key range (switched off, see SPLIT_OFF)."""
-    from paper_2608_26523_amd import binding as B
-    hq, T = 2, 1131
-    k_nope, k_rope, _ = _split_keys(T, hq, 60)
-    v = _rand((T, hq, 128), 0.1, 61)
-    q = _rand((131, hq, 192), 0.1, 62)
-    attn = _attn(hq, 131, T, splits=3)
-    attn.plan([0, 131], [0], [1000])
-    with pytest.raises(B.VppError) as e:
-        attn.run_mla(q, k_nope, k_rope, v)
-    assert e.value.status == B.VPP_ERR_UNSUPPORTED
-
-
 def test_split_keys_full_size_mla_chunk():
     """mla workload, chunk 8 (prefix 65536, 8192 queries, 128 heads)."""
     from paper_2608_26523_amd import workloads as W
@@ -133,3 +116,40 @@ def test_split_keys_full_size_mla_chunk():
     out_b, _ = attn.run_mla(q, k_nope, k_rope, v)
     torch.cuda.synchronize()
     assert torch.equal(out_a, out_b)
+
+
+def test_split_keys_full_size_long_chunk():
+    """long workload, last chunk (prefix 507904, 16384 queries, 128 heads, 4 splits):
+    the split keys as contiguous tensors and as strided views into the concatenated
+    keys (a 24 GiB span, so 64-bit address arithmetic carries in every copy stream)."""
+    from paper_2608_26523_amd import workloads as W
+    w = W.get("long")
+    c = W.num_chunks(w) - 1
+    t0, cu, kvs, pre = W.chunk_segments(w, c)
+    rows = int(pre[0]) + int(cu[-1])
+    print("case: long chunk", c, "rows", rows, "splits", w.num_splits, flush=True)
+    std = 1.0 / math.sqrt(w.dqk)
+    k_full = W.normal_bf16((rows, w.hkv, w.dqk), std, w.seed, w.index, "k", DEV)
+    k_full[:, 1:, 128:] = k_full[:, :1, 128:]          # one shared rope part per row
+    v = W.normal_bf16((rows, w.hkv, w.dv), std, w.seed, w.index, "v", DEV)
+    q = W.make_q_rows(w, DEV, t0, t0 + int(cu[-1]))
+    nope_view, rope_view = k_full[:, :, :128], k_full[:, 0, 128:]
+    assert nope_view.stride(0) == w.hkv * 192 and rope_view.stride(0) == w.hkv * 192
+    k_nope, k_rope = nope_view.contiguous(), rope_view.contiguous()
+    from paper_2608_26523_amd.attention import ChunkAttention
+    attn = ChunkAttention(w.hq, w.hkv, w.dqk, w.dv, max_chunk_tokens=w.chunk, max_kv_len=rows,
+                          num_splits=w.num_splits)
+    attn.plan(cu, kvs, pre)
+    assert attn.info().num_splits == w.num_splits
+    tok = int(cu[-1])
+    lse = [torch.full((w.hq, tok), float(i), dtype=torch.float32, device=DEV) for i in range(3)]
+    out_a, _ = attn.run(q, k_full, v, lse=lse[0])
+    out_b, _ = attn.run_mla(q, nope_view, rope_view, v, lse=lse[1])
+    out_c, _ = attn.run_mla(q, k_nope, k_rope, v, lse=lse[2])
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(out_a).all())
+    assert torch.equal(out_a, out_b), "strided split keys differ from the concatenated keys"
+    assert torch.equal(out_a, out_c), "contiguous split keys differ from the concatenated keys"
+    assert torch.equal(lse[0], lse[1]) and torch.equal(lse[0], lse[2])
+    del k_full, k_nope, k_rope, v, q
+    torch.cuda.empty_cache()
