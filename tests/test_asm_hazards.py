@@ -11,6 +11,11 @@ whenever the low half wraps):
 * source: every asm template that runs a scalar ALU instruction declares "scc";
 * assembly: in the device code of every build part, no instruction that reads
   SCC takes it from before an asm block that writes SCC.
+
+The query rows are loaded by asm straight into AGPRs, and a later asm waits
+for them (vmcnt). The compiler sees the registers as written when the load
+statement ends, so the assembly check also makes sure that no instruction
+touches them before that wait.
 """
 import os
 import re
@@ -92,6 +97,46 @@ def _scan(asm_text: str):
     return hits
 
 
+def _agprs(text: str):
+    regs = set()
+    for m in re.finditer(r"a\[(\d+):(\d+)\]", text):
+        regs.update(range(int(m.group(1)), int(m.group(2)) + 1))
+    for m in re.finditer(r"\ba(\d+)\b", text):
+        regs.add(int(m.group(1)))
+    return regs
+
+
+def _scan_async_agpr(asm_text: str):
+    """(loads, instructions touching an AGPR of an asm global load before its vmcnt wait)."""
+    hits, pending, loads = [], set(), 0
+    in_asm, block = False, []
+    for n, line in enumerate(asm_text.splitlines(), 1):
+        if ";;#ASMSTART" in line:
+            in_asm, block = True, []
+            continue
+        if ";;#ASMEND" in line:
+            in_asm = False
+            for ins in block:
+                if ins.startswith("global_load") and " a" in ins.split(",")[0]:
+                    loads += 1
+                    pending |= _agprs(ins.split(",")[0])
+                elif ins.startswith("s_waitcnt") and "vmcnt(0)" in ins:
+                    pending = set()
+            continue
+        code = line.split(";")[0].strip()
+        if in_asm:
+            if code:
+                block.append(code)
+            continue
+        if not code or code.endswith(":"):
+            continue
+        if code.startswith("s_waitcnt") and "vmcnt(0)" in code:
+            pending = set()
+        elif pending and _agprs(code) & pending:
+            hits.append((n, code))
+    return loads, hits
+
+
 def test_scan_finds_a_planted_hazard():
     planted = "\n".join([
         "\ts_add_u32 s4, s4, s6",
@@ -103,10 +148,22 @@ def test_scan_finds_a_planted_hazard():
     assert len(_scan(planted)) == 1
     fixed = planted.replace("\ts_addc_u32", "\ts_add_u32 s8, s8, s9\n\ts_addc_u32")
     assert _scan(fixed) == []
+    early = "\n".join([
+        "\t;;#ASMSTART",
+        "\tglobal_load_dwordx4 a[4:7], v2, off",
+        "\t;;#ASMEND",
+        "\tv_accvgpr_read_b32 v9, a5",
+        "\t;;#ASMSTART",
+        "\ts_waitcnt vmcnt(0)",
+        "\t;;#ASMEND",
+        "\tv_accvgpr_read_b32 v10, a6",
+    ])
+    loads, hits = _scan_async_agpr(early)
+    assert loads == 1 and [h[1] for h in hits] == ["v_accvgpr_read_b32 v9, a5"]
 
 
 @pytest.mark.skipif(not os.path.exists(BLD.hipcc()), reason="hipcc not installed")
-def test_device_code_keeps_scc_across_asm(tmp_path):
+def test_device_code_asm_hazards(tmp_path):
     base = [BLD.hipcc()] + [f for f in BLD.HIPCC_FLAGS if f not in ("-shared", "-Wall")] + ["-I", BLD.INCLUDE]
     procs = []
     for part in BLD.PARTS:
@@ -121,4 +178,7 @@ def test_device_code_keeps_scc_across_asm(tmp_path):
         assert "buffer_load_dwordx4" in text and ";;#ASMSTART" in text
         hits = _scan(text)
         assert hits == [], "part %d: SCC read after an SCC-writing asm block: %s" % (part, hits[:5])
+        loads, early = _scan_async_agpr(text)
+        assert loads > 0, "part %d: no asm query loads found" % part
+        assert early == [], "part %d: query AGPRs used before their load completed: %s" % (part, early[:5])
     shutil.rmtree(tmp_path, ignore_errors=True)
