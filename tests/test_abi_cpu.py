@@ -233,3 +233,39 @@ def test_tile_rows_follow_chunk_size(monkeypatch):
     # every item's rows fit the tile
     for n in (1, 127, 128, 129, 300):
         check_plan(cfg(hq=4, hkv=2), [0, n], [0], [17])
+
+
+# Random segment mixes through the same invariant checks: empty and ragged
+# segments, long prefixes, forced and automatic splits, every head-dim pair.
+from hypothesis import HealthCheck, given, settings, strategies as st  # noqa: E402
+
+_HEADS = [(4, 4), (8, 2), (32, 8), (128, 128)]
+_DIMS = [(64, 64), (128, 128), (192, 128)]
+
+
+@st.composite
+def _segment_mix(draw):
+    n = draw(st.integers(1, 8))
+    lens = draw(st.lists(st.integers(0, 700), min_size=n, max_size=n))
+    if sum(lens) == 0:
+        lens[0] = draw(st.integers(1, 700))
+    prefixes = draw(st.lists(st.integers(0, 300000), min_size=n, max_size=n))
+    starts, row = [], 0
+    for ln, p in zip(lens, prefixes):       # each segment's own cache region
+        starts.append(row)
+        row += p + ln + draw(st.integers(0, 50))
+    hq, hkv = draw(st.sampled_from(_HEADS))
+    dqk, dv = draw(st.sampled_from(_DIMS))
+    splits = draw(st.sampled_from([-1, 1, 2, 3, 7, 16]))
+    return lens, prefixes, starts, row, (hq, hkv, dqk, dv), splits
+
+
+@settings(max_examples=150, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(_segment_mix())
+def test_plan_random_segment_mixes(mix):
+    lens, prefixes, starts, rows, (hq, hkv, dqk, dv), splits = mix
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    c = cfg(hq=hq, hkv=hkv, dqk=dqk, dv=dv, max_tok=int(cu[-1]), max_kv=max(rows, 1), splits=splits)
+    info = check_plan(c, cu, starts, prefixes)
+    if splits > 0:
+        assert info.num_splits == splits

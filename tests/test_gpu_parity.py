@@ -268,3 +268,40 @@ def test_tile_variants_split(nb, dims, monkeypatch):
     attn = _attn(hq, hkv, dqk, dv, rows, T, splits=3)
     _full_check(attn, q, k, v, cu, [0], [prefix], what="split nb=%d dims=%s" % (nb, dims))
     assert attn.info().num_splits == 3
+
+
+def _random_mix(seed):
+    """A seeded random chunk: 1-4 segments (empty ones allowed), ragged lengths,
+    prefixes up to 1500 rows, one of the head and dim pairs, a split count."""
+    rng = np.random.default_rng(seed)
+    heads = [(4, 4), (8, 2), (6, 3), (2, 1)][rng.integers(4)]
+    dims = [(64, 64), (128, 128), (192, 128)][rng.integers(3)]
+    n = int(rng.integers(1, 5))
+    segs, row = [], 0
+    for _ in range(n):
+        ln = int(rng.integers(0, 300)) if rng.random() > 0.15 else 0
+        p = int(rng.integers(0, 1500)) if rng.random() > 0.25 else 0
+        segs.append((row, p, ln))
+        row += p + ln + int(rng.integers(0, 40))
+    if sum(s[2] for s in segs) == 0:
+        segs[0] = (segs[0][0], segs[0][1], 1 + int(rng.integers(0, 200)))
+        row = max(row, segs[0][0] + segs[0][1] + segs[0][2])
+    splits = [-1, 1, 2, 3][rng.integers(4)]
+    nb = [1, 2][rng.integers(2)]
+    return heads, dims, segs, row, splits, nb
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_mixes(seed, monkeypatch):
+    (hq, hkv), (dqk, dv), segs, T, splits, nb = _random_mix(seed)
+    monkeypatch.setenv("VPP_NB", str(nb))
+    tok = sum(s[2] for s in segs)
+    std = 1.0 / math.sqrt(dqk)
+    q = _rand((tok, hq, dqk), std, 400 + seed)
+    k = _rand((T, hkv, dqk), std, 500 + seed)
+    v = _rand((T, hkv, dv), std, 600 + seed)
+    cu = np.cumsum([0] + [s[2] for s in segs])
+    attn = _attn(hq, hkv, dqk, dv, tok, T, splits=splits)
+    _full_check(attn, q, k, v, cu, [s[0] for s in segs], [s[1] for s in segs],
+                what="random mix %d: heads %d/%d dims %d/%d nb %d splits %d segs %s" %
+                (seed, hq, hkv, dqk, dv, nb, splits, segs))
