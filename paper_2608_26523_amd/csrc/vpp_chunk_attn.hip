@@ -386,20 +386,18 @@ struct Schedule {
     }
 };
 
-// The MFMAs are written as inline asm so that each operand stays in the
-// register file it belongs to for the whole loop: Q and the O accumulators in
-// AGPRs (only MFMAs touch them), S and P in VGPRs (the softmax reads and
-// writes them). The compiler cannot see the latency of these instructions, so
-// the schedule keeps the required distances itself: an S^T tile is read by
-// VALU code only in the next tile's step (after a barrier), O only after an
-// explicit drain, and the "s_nop 2" in front of an O^T MFMA covers a P operand
-// packed by VALU code just before it.
+// The S^T MFMAs are inline asm so that each operand stays in the register
+// file it belongs to for the whole loop: S in VGPRs (the softmax reads and
+// writes it in place) and Q in AGPRs (only MFMAs read it). The compiler cannot
+// see the latency of these instructions, so the schedule keeps the distance
+// itself: an S^T tile is read by VALU code only in the next tile's step (after
+// a barrier). The O^T MFMAs use the builtin, so the compiler tracks their
+// operand hazards (P packed by VALU code just before) and keeps O in AGPRs;
+// the asm that rescales O in place runs only after an explicit drain.
 #define MFMA_32x32x16_INIT(acc, a, b) \
     asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b))
 #define MFMA_32x32x16_ACC(acc, a, b) \
     asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b))
-#define MFMA_32x32x16_PV(acc, a, b) \
-    asm volatile("s_nop 2\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b))
 
 __device__ __forceinline__ void mfma_drain() {
     // longer than the longest MFMA result latency: 3 x 16 wait states
