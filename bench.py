@@ -95,6 +95,26 @@ def measured_traffic(workload):
     return None
 
 
+def measured_traffic_chunks(workload):
+    """HBM bytes of each chunk's attention launch from the same summary (chunk -> bytes);
+    None unless it was taken on the kernel source that is here now."""
+    import hashlib
+    try:
+        with open(KERNEL_SRC, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()[:16]
+        out = {}
+        with open(TRAFFIC_FILE) as f:
+            for ln in f:
+                parts = ln.split()
+                if len(parts) == 5 and parts[0] == "traffic_chunk" and parts[1] == workload:
+                    if parts[2] != sha:
+                        return None
+                    out[int(parts[3])] = float(parts[4])
+        return out or None
+    except OSError:
+        return None
+
+
 def gemm_reference(dev, n=16384, reps=10):
     """Rate of the platform's own bf16 GEMM (hipBLASLt through torch.matmul) on operands of
     the same kind as the attention inputs (i.i.d. normal) and on zeros. MFMA throughput on
@@ -253,8 +273,11 @@ def measured_mfma(workload):
                 parts = ln.split()
                 if len(parts) == 5 and parts[0] == "mfma" and parts[1] == workload and parts[2] == sha:
                     busy, mhz = float(parts[3]), float(parts[4])
+                    # dense bf16 MFMA peak at the clock the kernel actually ran: 256 CUs x
+                    # 4096 flop per clock (2.5 PFLOP/s at 2.4 GHz)
                     return {"busy": busy, "clock_mhz": mhz,
                             "busy_vs_peak_clock": round(busy * mhz / 2400.0, 4),
+                            "peak_at_clock_tflops": round(256 * 4096 * mhz * 1e6 / 1e12, 1),
                             "source": "rocprofv3 counters, profiles/attn_fwd_mfma_clock.md"}
     except OSError:
         return None
@@ -497,8 +520,18 @@ def main():
                       "min_ms": [round(min(x), 4) for x in per_chunk],
                       "cold_ms": [round(x, 4) for x in cold] if cold else None,
                       "tflops": [round(f / (m * 1e-3) / 1e12, 2) for f, m in zip(flops, med)],
+                      # algorithmic bytes over the median time; hbm_gbs: the counter-measured
+                      # bytes of the same chunk (committed summary, this kernel source) instead
+                      "alg_gbs": [round(b / (m * 1e-3) / 1e9, 1) for b, m in zip(nbytes, med)],
+                      "hbm_gbs": None,
                       "splits": splits, "fit": fit, "eq3_residual": eq3},
     }
+    tc = None if (args.paged or args.mla_split) else measured_traffic_chunks(w.name)
+    if tc is not None and all(c in tc for c in range(nchunks)):
+        res["per_chunk"]["hbm_gbs"] = [round(tc[c] / (m * 1e-3) / 1e9, 1) for c, m in enumerate(med)]
+    mu = res["roofline"].get("mfma_util")
+    if mu:
+        mu["frac_at_clock"] = round(achieved / mu["peak_at_clock_tflops"], 4)
     if paged is not None:
         # the last timed step's append kernels: HBM-bound, new K/V rows read and written once
         app_ms = [append_ev[c][0].elapsed_time(append_ev[c][1]) for c in range(nchunks)]

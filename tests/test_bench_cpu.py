@@ -58,7 +58,9 @@ def test_profile_readers_are_hash_gated(tmp_path, monkeypatch):
     import hashlib
     sha = hashlib.sha256(b"kernel source").hexdigest()[:16]
     traffic = tmp_path / "t.md"
-    traffic.write_text("x\n    traffic gqa %s 12345\n    traffic mla deadbeefdeadbeef 7\n" % sha)
+    traffic.write_text("x\n    traffic gqa %s 12345\n    traffic mla deadbeefdeadbeef 7\n"
+                       "    traffic_chunk gqa %s 0 100\n    traffic_chunk gqa %s 1 250\n"
+                       "    traffic_chunk mla deadbeefdeadbeef 0 9\n" % (sha, sha, sha))
     mfma = tmp_path / "m.md"
     mfma.write_text("    mfma gqa %s 0.5000 1800\n" % sha)
     monkeypatch.setattr(bench, "KERNEL_SRC", str(src))
@@ -66,9 +68,13 @@ def test_profile_readers_are_hash_gated(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "MFMA_FILE", str(mfma))
     assert bench.measured_traffic("gqa") == 12345.0
     assert bench.measured_traffic("mla") is None          # taken on another kernel source
+    assert bench.measured_traffic_chunks("gqa") == {0: 100.0, 1: 250.0}
+    assert bench.measured_traffic_chunks("mla") is None
     m = bench.measured_mfma("gqa")
     assert m["busy"] == 0.5 and m["clock_mhz"] == 1800.0
     assert m["busy_vs_peak_clock"] == pytest.approx(0.5 * 1800 / 2400)
+    # 256 CUs x 4096 flop per clock: 2.5 PFLOP/s at 2.4 GHz
+    assert m["peak_at_clock_tflops"] == pytest.approx(2516.6 * 1800 / 2400, abs=0.1)
     assert bench.measured_mfma("mla") is None
 
 
@@ -76,3 +82,7 @@ def test_committed_profiles_match_the_kernel_source():
     """The committed summaries were taken on the kernel source that is in the tree."""
     assert bench.measured_traffic("gqa") is not None and bench.measured_traffic("mla") is not None
     assert bench.measured_mfma("gqa") is not None and bench.measured_mfma("mla") is not None
+    from paper_2608_26523_amd import workloads as W
+    for name in ("gqa", "mla"):
+        tc = bench.measured_traffic_chunks(name)
+        assert tc is not None and sorted(tc) == list(range(W.num_chunks(W.get(name))))
