@@ -548,6 +548,8 @@ def main():
         res["roofline"]["gemm_ref"] = ref
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, q, k, v, nchunks)
+        # the oracle over the whole timed step, extrapolated from the sampled rate (not run)
+        res["cpu_baseline"]["extrapolated_step_s"] = round(total_flops / (res["cpu_baseline"]["value"] * 1e12), 1)
     print(json.dumps(res), flush=True)
 
 
