@@ -369,9 +369,15 @@ struct Schedule {
             for (int k = 0; k < A::N; ++k) n += done_at[k] <= s;
             atoms_end[s] = n;
         }
+        // The (rare) O rescale is a branch; it runs right after the finishing
+        // atoms. Atoms scheduled between it and the first O^T MFMA feed only code
+        // after the branch, and the compiler would sink them past it into one
+        // burst with no MFMA to hide under.
         rescale_before = NS;
+        for (int s = NS - 1; s >= 1; --s)
+            if (atoms_end[s - 1] >= A::EXP) rescale_before = s;
         for (int s = NS - 1; s >= 0; --s)
-            if (kind[s] == 1) rescale_before = s;
+            if (kind[s] == 1 && s < rescale_before) rescale_before = s;
     }
     // every O^T MFMA comes after the atoms it depends on; atoms run in order
     constexpr bool valid() const {
