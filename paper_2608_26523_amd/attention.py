@@ -34,7 +34,10 @@ class ChunkAttention:
                             softmax_scale=softmax_scale, causal=1,
                             max_chunk_tokens=max_chunk_tokens, max_segments=max_segments,
                             max_kv_len=max_kv_len, num_splits=num_splits)
-        self.device = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        dev = torch.device(device) if device is not None else torch.device("cuda")
+        if dev.type != "cuda":
+            raise ValueError("the workspace must be on a GPU, not %s" % dev)
+        self.device = dev if dev.index is not None else torch.device("cuda", torch.cuda.current_device())
         self._plan: Optional[int] = None
         self._ws: Optional[torch.Tensor] = None
         self.workspace_bytes = 0
@@ -76,17 +79,38 @@ class ChunkAttention:
         if t.stride(-1) != 1:
             raise ValueError("%s: last dimension must be contiguous" % name)
 
+    def _on_device(self, *named):
+        """Every tensor must live on the device that holds the plan's workspace."""
+        for t, name in named:
+            if t is not None and t.device != self.device:
+                raise ValueError("%s is on %s but the plan's workspace is on %s" % (name, t.device, self.device))
+
+    def _stream(self, stream, *allocated):
+        """The launch stream (default: torch's current stream). Memory this object
+        allocated on the current stream is recorded on another launch stream, so that
+        torch's allocator does not hand it out while the kernel may still use it."""
+        cur = torch.cuda.current_stream(self.device)
+        s = stream if stream is not None else cur
+        if s != cur:
+            for t in (self._ws,) + allocated:
+                if t is not None:
+                    t.record_stream(s)
+        return s
+
     def _io(self, q: torch.Tensor, out: Optional[torch.Tensor], lse: Optional[torch.Tensor]):
-        """Checks of q, out and lse shared by both run methods; allocates out if None."""
+        """Checks of q, out and lse shared by the run methods; allocates out if None
+        (the second value returned is that new tensor, else None)."""
         if self._plan is None:
             raise RuntimeError("plan() must be called before run()")
         c = self.cfg
         self._check(q, "q", torch.bfloat16, 3)
+        self._on_device((q, "q"), (out, "out"), (lse, "lse"))
         if q.shape[0] < self.tokens or q.shape[1] != c.num_q_heads or q.shape[2] != c.head_dim_qk:
             raise ValueError("q shape %s does not match the plan" % (tuple(q.shape),))
+        new_out = None
         if out is None:
-            out = torch.empty((self.tokens, c.num_q_heads, c.head_dim_v), dtype=torch.bfloat16,
-                              device=q.device)
+            out = new_out = torch.empty((self.tokens, c.num_q_heads, c.head_dim_v), dtype=torch.bfloat16,
+                                        device=q.device)
         self._check(out, "out", torch.bfloat16, 3)
         if out.shape[0] < self.tokens or out.shape[1] != c.num_q_heads or out.shape[2] != c.head_dim_v:
             raise ValueError("out shape %s does not match the plan" % (tuple(out.shape),))
@@ -97,7 +121,7 @@ class ChunkAttention:
             if lse.shape[0] != c.num_q_heads or lse.shape[1] < self.tokens:
                 raise ValueError("lse shape %s does not match the plan" % (tuple(lse.shape),))
             lse_ptr, lse_sh = lse.data_ptr(), lse.stride(0)
-        return out, lse_ptr, lse_sh
+        return out, lse_ptr, lse_sh, new_out
 
     def run(self, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
             out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
@@ -109,7 +133,7 @@ class ChunkAttention:
         element [h, r] is chunk row r of head h (e.g. a column slice of a
         [Hq, seq] tensor), or None.
         """
-        out, lse_ptr, lse_sh = self._io(q, out, lse)
+        out, lse_ptr, lse_sh, new_out = self._io(q, out, lse)
         c = self.cfg
         self._check(k_cache, "k_cache", torch.bfloat16, 3)
         self._check(v_cache, "v_cache", torch.bfloat16, 3)
@@ -120,7 +144,8 @@ class ChunkAttention:
         if k_cache.shape[0] < self.max_row or v_cache.shape[0] < self.max_row:
             raise ValueError("the planned chunk reads cache rows up to %d but the caches hold "
                              "%d/%d rows" % (self.max_row, k_cache.shape[0], v_cache.shape[0]))
-        s = stream if stream is not None else torch.cuda.current_stream(q.device)
+        self._on_device((k_cache, "k_cache"), (v_cache, "v_cache"))
+        s = self._stream(stream, new_out)
         B.vpp_chunk_attn_run(self._plan,
                              q.data_ptr(), q.stride(0), q.stride(1),
                              k_cache.data_ptr(), k_cache.stride(0), k_cache.stride(1),
@@ -135,7 +160,7 @@ class ChunkAttention:
                 stream: Optional[torch.cuda.Stream] = None):
         """Like ``run`` with the keys split as in the MLA models: k_nope [rows, Hkv, 128] per
         head and k_rope [rows, 64] shared by all heads (head dims (192, 128) only)."""
-        out, lse_ptr, lse_sh = self._io(q, out, lse)
+        out, lse_ptr, lse_sh, new_out = self._io(q, out, lse)
         c = self.cfg
         if c.head_dim_qk != 192 or c.head_dim_v != 128:
             raise ValueError("the split key layout needs head dims (192, 128)")
@@ -149,7 +174,8 @@ class ChunkAttention:
             raise ValueError("v_cache shape %s does not match the config" % (tuple(v_cache.shape),))
         if min(k_nope.shape[0], k_rope.shape[0], v_cache.shape[0]) < self.max_row:
             raise ValueError("the planned chunk reads cache rows up to %d" % self.max_row)
-        s = stream if stream is not None else torch.cuda.current_stream(q.device)
+        self._on_device((k_nope, "k_nope"), (k_rope, "k_rope"), (v_cache, "v_cache"))
+        s = self._stream(stream, new_out)
         B.vpp_chunk_attn_run_mla(self._plan,
                                  q.data_ptr(), q.stride(0), q.stride(1),
                                  k_nope.data_ptr(), k_nope.stride(0), k_nope.stride(1),
@@ -166,7 +192,7 @@ class ChunkAttention:
         """Like ``run`` over a paged cache: k_pages [pages, page_size, Hkv, dqk], v_pages
         [pages, page_size, Hkv, dv] bf16; block_table int32 [segments, pages_per_row] on the
         device (row s: the pages of segment s's request, in cache-row order)."""
-        out, lse_ptr, lse_sh = self._io(q, out, lse)
+        out, lse_ptr, lse_sh, new_out = self._io(q, out, lse)
         c = self.cfg
         self._check(k_pages, "k_pages", torch.bfloat16, 4)
         self._check(v_pages, "v_pages", torch.bfloat16, 4)
@@ -186,7 +212,8 @@ class ChunkAttention:
         if need > block_table.shape[1] * page:
             raise ValueError("the planned chunk reads cache rows up to %d but a block-table row maps "
                              "%d" % (need, block_table.shape[1] * page))
-        s = stream if stream is not None else torch.cuda.current_stream(q.device)
+        self._on_device((k_pages, "k_pages"), (v_pages, "v_pages"), (block_table, "block_table"))
+        s = self._stream(stream, new_out)
         B.vpp_chunk_attn_run_paged(self._plan,
                                    q.data_ptr(), q.stride(0), q.stride(1),
                                    k_pages.data_ptr(), k_pages.stride(0), k_pages.stride(1), k_pages.stride(2),
@@ -220,6 +247,9 @@ def kv_append_paged(k_new: torch.Tensor, v_new: torch.Tensor, k_pages: torch.Ten
         ChunkAttention._check(t, name, torch.bfloat16, 3)
     for t, name in ((k_pages, "k_pages"), (v_pages, "v_pages")):
         ChunkAttention._check(t, name, torch.bfloat16, 4)
+    for t, name in ((v_new, "v_new"), (k_pages, "k_pages"), (v_pages, "v_pages")):
+        if t.device != k_new.device:
+            raise ValueError("%s is on %s, k_new on %s" % (name, t.device, k_new.device))
     if slot_mapping.dtype != torch.int64 or slot_mapping.dim() != 1 or slot_mapping.device != k_new.device \
             or slot_mapping.stride(0) != 1:
         raise ValueError("slot_mapping must be a contiguous int64 vector on the GPU")

@@ -305,3 +305,37 @@ def test_random_mixes(seed, monkeypatch):
     _full_check(attn, q, k, v, cu, [s[0] for s in segs], [s[1] for s in segs],
                 what="random mix %d: heads %d/%d dims %d/%d nb %d splits %d segs %s" %
                 (seed, hq, hkv, dqk, dv, nb, splits, segs))
+
+
+def test_side_stream_and_growing_workspace():
+    """Runs on a side stream (default priority), with a re-plan that grows the workspace in
+    between, give the same bits as runs on torch's current stream; device="cuda" without an
+    index resolves to the current device."""
+    from paper_2608_26523_amd.attention import ChunkAttention
+    hq, hkv, d = 4, 2, 128
+    std = 1.0 / math.sqrt(d)
+    T = 3000
+    k = _rand((T, hkv, d), std, 700)
+    v = _rand((T, hkv, d), std, 701)
+    q = _rand((1024, hq, d), std, 702)
+    cases = [([0, 200], [0], [100]), ([0, 1024], [0], [1900])]   # the second needs more workspace
+    ref = []
+    a_ref = ChunkAttention(hq, hkv, d, d, max_chunk_tokens=1024, max_kv_len=T, device="cuda")
+    assert a_ref.device == torch.device("cuda", torch.cuda.current_device())
+    for cu, ks, pl in cases:
+        a_ref.plan(cu, ks, pl)
+        ref.append(a_ref.run(q[:cu[-1]], k, v)[0].clone())
+    side = torch.cuda.Stream()
+    a = ChunkAttention(hq, hkv, d, d, max_chunk_tokens=1024, max_kv_len=T)
+    outs = []
+    for cu, ks, pl in cases:
+        ws_before = a.workspace_bytes
+        a.plan(cu, ks, pl)
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            o, _ = a.run(q[:cu[-1]], k, v, stream=side)
+        outs.append(o)
+    assert a.workspace_bytes > ws_before
+    torch.cuda.synchronize()
+    for o, r in zip(outs, ref):
+        assert torch.equal(o, r)
