@@ -106,7 +106,7 @@ def test_mla_chunks():
 
 
 def test_long_split_chunks():
-    infos = _single_request("long", [0, 4, 31])
+    infos = _single_request("long", [0, 4, 16, 31])
     assert infos[-1].num_splits == 4
 
 
