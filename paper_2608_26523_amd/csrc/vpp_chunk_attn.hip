@@ -52,7 +52,7 @@ constexpr int NTHREADS = 64 * NWAVES;
 constexpr int MAX_SPLITS = 16;
 [[maybe_unused]] constexpr int STAGING_SLOTS = 4;
 // cache layouts (kernel template argument KVM)
-constexpr int KV_CONTIG = 0, KV_PAGED = 1, KV_ROPE = 2;
+[[maybe_unused]] constexpr int KV_CONTIG = 0, KV_PAGED = 1, KV_ROPE = 2;
 // split key layout: granules of the per-head and of the shared part of a K row
 constexpr int NOPE_GR = 16, ROPE_GR = 8;
 // Lazy rescale: the running max used for exp2 is refreshed only when a row's
