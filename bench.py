@@ -15,7 +15,12 @@ least-squares fit t_k = a + b*k, the residual of the balance identity of Eq. (3)
 with HIP events on the launch stream) and the fp64 oracle's rate on the host
 cores over a bounded sample of the same workload.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload gqa|mla|long|mixed|tiny]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload long|mla|gqa|mixed|tiny]
+
+The default workload is the longest single-GPU one: a 524288-token prompt in 32 chunks of
+16384 queries, 128 heads of the MLA shape (dqk 192, dv 128), the key range split four ways
+with an lse merge; its chunks with a prefix of 64K keys or more (chunks 4..31) are the ones
+the 60 %-of-peak target is stated on.
 """
 from __future__ import annotations
 
@@ -332,12 +337,17 @@ def cpu_baseline(w, q, k, v, chunks, budget_s=12.0):
                       "fp64, %s" % (done_items, kidx, int(pre[0]), elapsed, cpu_model())}
 
 
+def progress(msg):
+    """A progress line on stderr (the JSON result is the only line on stdout)."""
+    print("bench: " + msg, file=sys.stderr, flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=0)
     ap.add_argument("--warmup", type=int, default=-1)
-    ap.add_argument("--workload", default="gqa")
+    ap.add_argument("--workload", default="long")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemm-ref", action="store_true",
                     help="skip the library GEMM reference taken after the timed steps")
@@ -397,6 +407,8 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     q, k, v = W.make_inputs(w, dev)
+    torch.cuda.synchronize()
+    progress("%s inputs resident: q %s, k %s, v %s" % (w.name, tuple(q.shape), tuple(k.shape), tuple(v.shape)))
     S = q.shape[0]
     out = torch.empty((S, w.hq, w.dv), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((w.hq, S), dtype=torch.float32, device=dev)
@@ -460,14 +472,22 @@ def main():
         step(cold_ev)
         torch.cuda.synchronize()
         cold = [cold_ev[c][0].elapsed_time(cold_ev[c][1]) for c in range(nchunks)]
+        progress("cold step done (%.1f ms)" % sum(cold))
     for _ in range(max(0, warmup - 1)):
         step()
     torch.cuda.synchronize()
+    progress("%d warm-up step(s) done; timing %d step(s)" % (warmup, steps))
     ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
            for _ in range(nchunks)] for _ in range(steps)]
     t_start = time.perf_counter()
     for s in range(steps):
         step(ev[s])
+        if steps > 1 and w.name in ("long", "mixed"):
+            # the host waits for each step's last event so that the line prints when the
+            # step has finished; the next step's first launch then starts from an idle
+            # queue (one launch latency, ~0.1 ms of a step of seconds)
+            ev[s][-1][1].synchronize()
+            progress("timed step %d/%d done" % (s + 1, steps))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
 

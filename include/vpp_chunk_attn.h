@@ -29,7 +29,10 @@
  *   lse      fp32 [Hq][...]              element h*lse_stride_head + r is chunk
  *                                        row r, head h (nullable)
  * Strides are in elements; the last dimension is contiguous; base pointers and
- * the token/head strides are multiples of 8 elements (16 bytes). Query head h
+ * the token/head strides are multiples of 8 elements (16 bytes). Strides are
+ * below 2^25 elements, and the cache row strides (k_stride_tok, v_stride_tok,
+ * and kr_stride_tok of the split key layout) below 2^24: one 64-row key tile
+ * must span less than 2^31 bytes. Larger strides are VPP_ERR_INVALID_ARG. Query head h
  * reads kv head h / (Hq / Hkv) (contiguous groups: grouped-query attention;
  * Hq == Hkv is multi-head attention, which is also how the MLA models of
  * section 6.1 are run in prefill, with dqk = 192 and dv = 128).
@@ -90,8 +93,10 @@ typedef struct vpp_chunk_attn_plan_s* vpp_chunk_attn_plan_t;
  *
  * *inout_plan == NULL creates a plan (owned by the library until
  * vpp_chunk_attn_destroy); a non-NULL plan is refilled in place with the same
- * config (cfg may be NULL then) -- waiting first, on the host, for the device
- * to finish reading the work list of the plan's previous run.
+ * config (cfg may be NULL then). Refilling never blocks: each run copies the
+ * work list to the device from a pinned staging slot of its own (a ring of 4
+ * per plan), and only a run that reuses a slot whose earlier copy is still in
+ * flight waits, on the host, for that copy.
  * *workspace_bytes receives the bytes of device workspace vpp_chunk_attn_run
  * needs for this plan (always > 0). The arrays are not retained.
  */
@@ -224,12 +229,13 @@ const char* vpp_status_str(vpp_status_t status);
 typedef struct {
     int32_t num_tiles;        /* query tiles (per head) in the chunk               */
     int32_t num_splits;       /* split count chosen (1 = no merge pass)            */
-    int32_t num_work_items;   /* tiles x splits: workgroups per head               */
+    int32_t num_work_items;   /* work-list entries: two per slot                   */
     int32_t block_m;          /* query rows per tile                               */
     int32_t block_n;          /* keys per inner step                               */
     int32_t num_tokens;       /* cu_q[n]                                           */
     int64_t workspace_bytes;  /* same value vpp_chunk_attn_plan returned           */
     double pairs;             /* visible (query, key) pairs per head               */
+    int32_t num_slots;        /* work slots = workgroups per head of the launch    */
 } vpp_chunk_attn_plan_info_t;
 
 vpp_status_t vpp_chunk_attn_plan_info(vpp_chunk_attn_plan_t plan,
@@ -248,7 +254,11 @@ typedef struct {
 } vpp_chunk_attn_work_item_t;
 
 /* Copy up to `capacity` work items of the plan, in launch order; *count gets
- * the plan's item count. */
+ * the plan's item count. Entries 2m and 2m+1 form work slot m, which one
+ * workgroup per head runs: the first entry's tile with its keys ascending, then
+ * the second's (the partner tile from the other end of the same segment, in the
+ * same split piece) with its keys descending. A second entry with nrows = 0 is
+ * empty. Every (tile, split piece) appears exactly once. */
 vpp_status_t vpp_chunk_attn_plan_items(vpp_chunk_attn_plan_t plan,
                                        vpp_chunk_attn_work_item_t* items,
                                        int32_t capacity, int32_t* count);

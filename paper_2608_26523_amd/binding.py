@@ -60,6 +60,7 @@ class PlanInfo(ctypes.Structure):
         ("num_tokens", ctypes.c_int32),
         ("workspace_bytes", ctypes.c_int64),
         ("pairs", ctypes.c_double),
+        ("num_slots", ctypes.c_int32),
     ]
 
 

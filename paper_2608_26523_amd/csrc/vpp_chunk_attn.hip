@@ -129,7 +129,8 @@ struct AttnArgs {
     float* lse;  // fp32, h*lse_sh + row (nullable); split mode: partials [splits][Hq][tokens]
     // element strides (the host checks that they fit in 31 bits)
     int32_t q_st, q_sh, k_st, k_sh, v_st, v_sh, o_st, o_sh, lse_sh;
-    int32_t num_items;
+    int32_t num_slots;  // work slots (two work-list entries each); the grid is num_slots x num_heads
+    int32_t num_entries;  // work-list entries: no entry at or past this index is read
     int32_t num_heads;
     int32_t group;     // Hq / Hkv
     int32_t tokens;    // chunk rows (partial layout)
@@ -239,19 +240,19 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-// Launch-order index -> (item, head). With remapping on, the hardware's
+// Launch-order index -> (slot, head). With remapping on, the hardware's
 // round-robin placement of consecutive workgroups on the 8 XCDs is undone so
-// that each XCD runs a contiguous run of logical work (the tiles of the same
+// that each XCD runs a contiguous run of logical work (the slots of the same
 // heads, which read the same K/V through that XCD's L2).
-__device__ __forceinline__ void work_coords(const AttnArgs& a, int& item, int& head) {
-    const int64_t total = (int64_t)a.num_items * a.num_heads;
+__device__ __forceinline__ void work_coords(const AttnArgs& a, int& slot, int& head) {
+    const int64_t total = (int64_t)a.num_slots * a.num_heads;
     int64_t L = blockIdx.x;
     if (a.xcd_remap) {
         const int64_t per = total / 8;
         if (L < per * 8) L = (L % 8) * per + L / 8;
     }
-    head = (int)(L / a.num_items);
-    item = (int)(L % a.num_items);
+    head = (int)(L / a.num_slots);
+    slot = (int)(L % a.num_slots);
 }
 
 template <int DQK, int DV, int NB>
@@ -519,523 +520,548 @@ void attn_fwd_kernel(AttnArgs a) {
     char* const kbuf0 = smem;
     char* const vbuf0 = smem + 2 * T::K_BYTES;
 
-    int item_id, h;
-    work_coords(a, item_id, h);
-    // the work item is uniform: keep it in SGPRs (so buffer resources built
-    // from it are scalar too)
-    WorkItem it = a.items[item_id];
-    it.row0 = __builtin_amdgcn_readfirstlane(it.row0);
-    it.nrows = __builtin_amdgcn_readfirstlane(it.nrows);
-    it.pos0 = __builtin_amdgcn_readfirstlane(it.pos0);
-    it.key_begin = __builtin_amdgcn_readfirstlane(it.key_begin);
-    it.key_end = __builtin_amdgcn_readfirstlane(it.key_end);
-    it.split = __builtin_amdgcn_readfirstlane(it.split);
-    it.kv_base = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(it.kv_base >> 32)) << 32) |
-                           (uint32_t)__builtin_amdgcn_readfirstlane((int)it.kv_base));
-    const int hk = h / a.group;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS bases stay scalar
-    const int lr = lane & 31;
-    const int lg = lane >> 5;
+    int slot, h;
+    work_coords(a, slot, h);
+    // A slot holds up to two tiles: the first runs its key range ascending, the
+    // second (if any) descending; an empty second entry has no rows.
+#pragma nounroll
+    for (int sub = 0; sub < 2; ++sub) {
+        const int item_id = 2 * slot + sub;
+        if (item_id >= a.num_entries) break;
+        // the work item is uniform: keep it in SGPRs (so buffer resources built
+        // from it are scalar too)
+        WorkItem it = a.items[item_id];
+        it.row0 = __builtin_amdgcn_readfirstlane(it.row0);
+        it.nrows = __builtin_amdgcn_readfirstlane(it.nrows);
+        it.pos0 = __builtin_amdgcn_readfirstlane(it.pos0);
+        it.key_begin = __builtin_amdgcn_readfirstlane(it.key_begin);
+        it.key_end = __builtin_amdgcn_readfirstlane(it.key_end);
+        it.split = __builtin_amdgcn_readfirstlane(it.split);
+        it.kv_base = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(it.kv_base >> 32)) << 32) |
+                               (uint32_t)__builtin_amdgcn_readfirstlane((int)it.kv_base));
+        if (it.nrows == 0) break;
+        // every wave is done with the LDS tiles of the slot's previous tile before
+        // this tile's first copies overwrite them
+        lds_barrier();
+        const int hk = h / a.group;
+        const int tid = threadIdx.x;
+        const int lane = tid & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS bases stay scalar
+        const int lr = lane & 31;
+        const int lg = lane >> 5;
 
-    const int kb = it.key_begin, ke = it.key_end;
-    // contiguous cache: the request's row 0 of head hk; paged: page 0's row 0
-    const int64_t cache_row0 = PAGED ? 0 : it.kv_base;
-    const u16* kbase = a.k + cache_row0 * a.k_st + (int64_t)hk * a.k_sh;
-    const u16* vbase = a.v + cache_row0 * a.v_st + (int64_t)hk * a.v_sh;
-    const int ntiles = (ke - kb + BN - 1) / BN;
-    // paged cache: this segment's block-table row and the cache row of key 0
-    const int32_t* bt_row = PAGED ? a.block_table + (int64_t)(int32_t)(it.kv_base >> 32) * a.bt_st : nullptr;
-    const int kv_off = PAGED ? (int)(uint32_t)it.kv_base : 0;
-    const int pmask = PAGED ? (1 << a.page_shift) - 1 : 0;
-    const int last_row = kv_off + ke - 1;  // page reads past the key range are clamped here
-    auto clamp_page = [&](int pg) { return (int)min((uint32_t)pg, (uint32_t)(a.num_pages - 1)); };
-    auto page_of = [&](int row) {  // synchronous lookup (prologue)
-        return clamp_page(__builtin_amdgcn_readfirstlane(bt_row[min(row, last_row) >> a.page_shift]));
-    };
-    // first element of the tile of keys starting at kt
-    auto tile_src = [&](const u16* base, int64_t page_st, int64_t row_st, int kt) -> const u16* {
-        if constexpr (PAGED) {
-            const int row = kv_off + kt;
-            return base + (int64_t)page_of(row) * page_st + (int64_t)(row & pmask) * row_st;
-        } else {
-            return base + (int64_t)kt * row_st;
-        }
-    };
-
-    // This lane's NB query rows (one per 32-column block of S^T), as B
-    // operands in AGPRs. Rows past the tile re-read its last row (their results
-    // are never stored), so every load stays inside q.
-    bf16x8 qf[NB][KS];
-    int qlim[NB];   // last key position the row may see, minus lg*4 (see masking)
-    bool qvalid[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const int rloc = wave * WROWS + nb * 32 + lr;
-        qvalid[nb] = rloc < it.nrows;
-        qlim[nb] = min(it.pos0 + rloc, ke - 1) - lg * 4;
-        const u16* qp = a.q + (int64_t)(it.row0 + min(rloc, it.nrows - 1)) * a.q_st + (int64_t)h * a.q_sh + lg * 8;
-        load_q_agpr<KS>(qf[nb], qp);
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    const int wave_first = it.pos0 + wave * WROWS;
-
-    // Global->LDS copy of one tile through a buffer resource whose base is the
-    // tile's first key row and whose size ends at the last key of the range:
-    // rows past the range read as zeros (buffer range check), so the last tile
-    // needs no special case. Per-lane byte offsets are fixed for the kernel.
-    // Split key layout: the K tile is two LDS regions, the per-head part
-    // [BN][NOPE_GR] granules then the shared part [BN][ROPE_GR], each filled by
-    // its own copies (a copy instruction has one source) and swizzled for its
-    // own row width; the first NOPE_LOADS copies read k_nope, the rest k_rope.
-    constexpr int NOPE_LOADS = BN * NOPE_GR / NTHREADS;
-    constexpr int NOPE_BYTES = BN * NOPE_GR * 16;
-    uint32_t k_src[T::K_LOADS], v_src[T::V_LOADS];
-#pragma unroll
-    for (int t = 0; t < T::K_LOADS; ++t) {
-        if constexpr (ROPE) {
-            if (t < NOPE_LOADS) {
-                const int slot = t * NTHREADS + tid;
-                const int row = slot / NOPE_GR, gs = slot % NOPE_GR;
-                k_src[t] = (uint32_t)(row * (int)a.k_st + kswz<NOPE_GR>(row, gs) * 8) * 2u;
+        const int kb = it.key_begin, ke = it.key_end;
+        // contiguous cache: the request's row 0 of head hk; paged: page 0's row 0
+        const int64_t cache_row0 = PAGED ? 0 : it.kv_base;
+        const u16* kbase = a.k + cache_row0 * a.k_st + (int64_t)hk * a.k_sh;
+        const u16* vbase = a.v + cache_row0 * a.v_st + (int64_t)hk * a.v_sh;
+        const int ntiles = (ke - kb + BN - 1) / BN;
+        // key tiles sit at kb + m*BN (m = 0 .. ntiles-1) in both directions; visit j
+        // of the tile loop reads the tile at kt_first + j*dkt
+        const bool rev = sub != 0;
+        const int dkt = rev ? -BN : BN;
+        const int kt_first = rev ? kb + (ntiles - 1) * BN : kb;
+        // paged cache: this segment's block-table row and the cache row of key 0
+        const int32_t* bt_row = PAGED ? a.block_table + (int64_t)(int32_t)(it.kv_base >> 32) * a.bt_st : nullptr;
+        const int kv_off = PAGED ? (int)(uint32_t)it.kv_base : 0;
+        const int pmask = PAGED ? (1 << a.page_shift) - 1 : 0;
+        const int last_row = kv_off + ke - 1;  // page reads past the key range are clamped here
+        auto clamp_page = [&](int pg) { return (int)min((uint32_t)pg, (uint32_t)(a.num_pages - 1)); };
+        auto page_of = [&](int row) {  // synchronous lookup (prologue)
+            return clamp_page(__builtin_amdgcn_readfirstlane(bt_row[min(row, last_row) >> a.page_shift]));
+        };
+        // first element of the tile of keys starting at kt
+        auto tile_src = [&](const u16* base, int64_t page_st, int64_t row_st, int kt) -> const u16* {
+            if constexpr (PAGED) {
+                const int row = kv_off + kt;
+                return base + (int64_t)page_of(row) * page_st + (int64_t)(row & pmask) * row_st;
             } else {
-                const int slot = (t - NOPE_LOADS) * NTHREADS + tid;
-                const int row = slot / ROPE_GR, gs = slot % ROPE_GR;
-                k_src[t] = (uint32_t)(row * (int)a.kr_st + kswz<ROPE_GR>(row, gs) * 8) * 2u;
+                return base + (int64_t)kt * row_st;
             }
-        } else {
-            const int slot = t * NTHREADS + tid;
-            const int row = slot / T::KGR, gs = slot % T::KGR;
-            k_src[t] = (uint32_t)(row * (int)a.k_st + kswz<T::KGR>(row, gs) * 8) * 2u;
-        }
-    }
-#pragma unroll
-    for (int t = 0; t < T::V_LOADS; ++t) {
-        const int slot = t * NTHREADS + tid;
-        const int row = slot / T::VGR, gs = slot % T::VGR;
-        v_src[t] = (uint32_t)(row * (int)a.v_st + vswz<T::VGR>(row, gs) * 8) * 2u;
-    }
-    // resources over the rows [kt, min(kt + BN, ke)) (none when kt >= ke)
-    auto k_rsrc = [&](int kt) {
-        return make_rsrc(tile_src(kbase, a.k_sp, a.k_st, kt), max(0, min(BN, ke - kt)) * (int)a.k_st * 2);
-    };
-    // the shared key part of the same rows (split layout; one row per key, no head)
-    const u16* rbase = ROPE ? a.k_rope + cache_row0 * a.kr_st : nullptr;
-    auto kr_rsrc = [&](int kt) {
-        return make_rsrc(rbase + (int64_t)kt * a.kr_st, max(0, min(BN, ke - kt)) * (int)a.kr_st * 2);
-    };
-    auto v_rsrc = [&](int kt) {
-        return make_rsrc(tile_src(vbase, a.v_sp, a.v_st, kt), max(0, min(BN, ke - kt)) * (int)a.v_st * 2);
-    };
-    const uint32_t lds_wave = (uint32_t)(uintptr_t)(lds_void_t*)smem + (uint32_t)wave * 1024u;
-    // copy t of the K (V) tile into buffer B: LDS offset from this wave's base
-    auto load_k = [&](const i32x4& r, const i32x4& rr, auto B, auto TT) {
-        constexpr int t = decltype(TT)::value;
-        if constexpr (ROPE && t >= NOPE_LOADS) {
-            constexpr int off = decltype(B)::value * T::K_BYTES + NOPE_BYTES + (t - NOPE_LOADS) * NWAVES * 1024;
-            copy16_to_lds<off>(rr, lds_wave, k_src[t]);
-        } else {
-            constexpr int off = decltype(B)::value * T::K_BYTES + t * NWAVES * 1024;
-            copy16_to_lds<off>(r, lds_wave, k_src[t]);
-        }
-    };
-    auto load_v = [&](const i32x4& r, auto B, auto TT) {
-        constexpr int off = 2 * T::K_BYTES + decltype(B)::value * T::V_BYTES + decltype(TT)::value * NWAVES * 1024;
-        copy16_to_lds<off>(r, lds_wave, v_src[decltype(TT)::value]);
-    };
-    auto issue_k = [&](auto B, int kt) {
-        const i32x4 r = k_rsrc(kt);
-        const i32x4 rr = ROPE ? kr_rsrc(kt) : r;
-        static_for<T::K_LOADS>([&](auto TT) { load_k(r, rr, B, TT); });
-    };
-    auto issue_v = [&](auto B, int kt) {
-        const i32x4 r = v_rsrc(kt);
-        static_for<T::V_LOADS>([&](auto TT) { load_v(r, B, TT); });
-    };
-    if (ntiles > 0) {
-        issue_k(std::integral_constant<int, 0>(), kb);
-        issue_v(std::integral_constant<int, 0>(), kb);
-        if (ntiles > 1) issue_k(std::integral_constant<int, 1>(), kb + BN);
-    }
+        };
 
-    // Per-lane LDS byte offsets; the rest of each address is an immediate.
-    // K (A operand of S^T): row mb*32+lr, logical granule ks*2+lg; row & 15 and
-    // (row >> 1) & 7 depend only on lr. The swizzle touches the low 4 (or 3)
-    // bits of the granule index, so K_OFFS offsets cover every ks and the
-    // higher granule bits are an immediate.
-    // (split key layout: K_OFFS offsets for the per-head region, KR_OFFS for the
-    // shared one)
-    constexpr int K_OFFS = ROPE ? NOPE_GR / 2 : ((T::KGR % 16 == 0) ? 8 : 4);
-    constexpr int KR_OFFS = ROPE ? ROPE_GR / 2 : 1;
-    int k_off[K_OFFS], kr_off[KR_OFFS];
-#pragma unroll
-    for (int r = 0; r < K_OFFS; ++r) {
-        if constexpr (ROPE) k_off[r] = lr * (NOPE_GR * 16) + kswz<NOPE_GR>(lr, r * 2 + lg) * 16;
-        else k_off[r] = lr * (T::KGR * 16) + kswz<T::KGR>(lr, r * 2 + lg) * 16;
-    }
-#pragma unroll
-    for (int r = 0; r < KR_OFFS; ++r) kr_off[r] = ROPE ? lr * (ROPE_GR * 16) + kswz<ROPE_GR>(lr, r * 2 + lg) * 16 : 0;
-    // V^T (A operand of O^T) through ds_read_b64_tr_b16: 16-lane group q reads
-    // keys 4*(q>>1) + (j>>2) and value columns 16*(q&1) + 4*(j&3) .. +3, i.e.
-    // granule 4*d + (tr_col >> 3) of value block d; key & 3 = tr_key & 3.
-    const int tq = lane >> 4, tj = lane & 15;
-    const int tr_key = 4 * (tq >> 1) + (tj >> 2);
-    const int tr_col = 16 * (tq & 1) + 4 * (tj & 3);
-    int v_off[DB];
-#pragma unroll
-    for (int d = 0; d < DB; ++d)
-        v_off[d] = tr_key * (T::VGR * 16) + vswz<T::VGR>(tr_key, d * 4 + (tr_col >> 3)) * 16 + (tr_col & 7) * 2;
-
-    float m_run[NB];   // max used by exp2 (log2 units), refreshed lazily
-    float l_part[NB];  // this lane's share of the softmax denominator
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        m_run[nb] = -INFINITY;
-        l_part[nb] = 0.f;
-    }
-    f32x16 o[DB][NB];
-#pragma unroll
-    for (int d = 0; d < DB; ++d)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) o[d][nb][i] = 0.f;
-
-    auto load_kfrag = [&](const char* kt_buf, int ks, int mb) -> bf16x8 {
-        if constexpr (ROPE) {
-            const char* addr = ks < NOPE_GR / 2
-                                   ? kt_buf + mb * 32 * NOPE_GR * 16 + k_off[ks]
-                                   : kt_buf + NOPE_BYTES + mb * 32 * ROPE_GR * 16 + kr_off[ks - NOPE_GR / 2];
-            return __builtin_bit_cast(bf16x8, *(const u32x4*)addr);
-        } else {
-            const u32x4 raw = *(const u32x4*)(kt_buf + mb * 32 * T::KGR * 16 + (ks / K_OFFS) * (K_OFFS * 32) +
-                                              k_off[ks % K_OFFS]);
-            return __builtin_bit_cast(bf16x8, raw);
-        }
-    };
-    auto load_vfrag = [&](const char* vt, int mb, int hh, int d) -> bf16x8 {
-        bf16x8 af;
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const char* addr = vt + (mb * 32 + hh * 16 + half * 8) * T::VGR * 16 + v_off[d];
-            const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(addr));
-            const bf16x4 rb = __builtin_bit_cast(bf16x4, r);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) af[half * 4 + j] = rb[j];
-        }
-        return af;
-    };
-
-    // S^T = K Q^T for a whole tile (prologue only: no softmax to overlap with)
-    auto qk_all = [&](const char* kt_buf, f32x16 (&s)[2][NB]) {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
-                const bf16x8 af = load_kfrag(kt_buf, ks, mb);
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) {
-                    const bf16x8 bq = qf[nb][ks];
-                    if (ks == 0) MFMA_32x32x16_INIT(s[mb][nb], af, bq);
-                    else MFMA_32x32x16_ACC(s[mb][nb], af, bq);
-                }
-            }
-    };
-
-    // Running sources of the copies a step issues (K(t+2) and V(t+1)): scalar
-    // pointer and remaining row count, advanced by one tile per step.
-    const int k_row_bytes = (int)a.k_st * 2, v_row_bytes = (int)a.v_st * 2;
-    uint64_t k_next = PAGED ? 0 : (uint64_t)(uintptr_t)(kbase + (int64_t)(kb + 2 * BN) * a.k_st);
-    uint64_t v_next = PAGED ? 0 : (uint64_t)(uintptr_t)(vbase + (int64_t)(kb + BN) * a.v_st);
-    int k_rows = ke - kb - 2 * BN, v_rows = ke - kb - BN;
-    // split key layout: the shared part's running source (same rows as K)
-    const int kr_row_bytes = ROPE ? (int)a.kr_st * 2 : 0;
-    uint64_t kr_next = ROPE ? (uint64_t)(uintptr_t)(rbase + (int64_t)(kb + 2 * BN) * a.kr_st) : 0;
-    // paged cache: the page of the K tile a step copies is read one step ahead
-    // (raw, clamped at its use), and V(t+1) shares K(t+1)'s page
-    int pg_pending = 0, pg_prev = 0;
-    if constexpr (PAGED) {
-        if (ntiles > 0) {
-            pg_prev = page_of(kv_off + kb + BN);
-            pg_pending = bt_row[min(kv_off + kb + 2 * BN, last_row) >> a.page_shift];
-        }
-    }
-
-    // One key tile: mask S(t) if needed, then the scheduled mix of S(t+1)
-    // MFMAs, the softmax of S(t) and the O^T += V^T P^T MFMAs of tile t.
-    auto step = [&](auto P, auto HAS_NEXT, int t, f32x16 (&s_cur)[2][NB], f32x16 (&s_nxt)[2][NB]) {
-        constexpr int par = decltype(P)::value;
-        constexpr bool has_next = decltype(HAS_NEXT)::value;
-        const char* kt_nxt = kbuf0 + (1 - par) * T::K_BYTES;
-        const char* vt_cur = vbuf0 + par * T::V_BYTES;
-        const int kt = kb + t * BN;
-        wait_vmcnt<0>();
-        lds_barrier();  // K(t+1), V(t) are in LDS; every wave is done with K(t) and V(t-1)
-        // the next tiles' copies (K(t+2) into the K buffer just freed, V(t+1)
-        // into the V buffer just freed) are spread over the first slots. Past
-        // the last tile the resources are empty: the copies then only write
-        // zeros into buffers that no later step reads, and the step needs no
-        // branch around them.
-        if constexpr (PAGED) {
-            // the page read during the previous step is complete after the
-            // barrier; the empty asm pins its use here, before any LDS read of
-            // this step is in flight
-            int pg_k = clamp_page(__builtin_amdgcn_readfirstlane(pg_pending));
-            asm volatile("" : "+s"(pg_k) : : "memory");
-            const int row_k = kv_off + kt + 2 * BN;
-            k_next = (uint64_t)(uintptr_t)(kbase + (int64_t)pg_k * a.k_sp + (int64_t)(row_k & pmask) * a.k_st);
-            v_next = (uint64_t)(uintptr_t)(vbase + (int64_t)pg_prev * a.v_sp + (int64_t)((row_k - BN) & pmask) * a.v_st);
-            pg_prev = pg_k;
-            pg_pending = bt_row[min(row_k + BN, last_row) >> a.page_shift];
-        }
-        const int k_bytes = k_rows >= BN ? BN * k_row_bytes : (k_rows > 0 ? k_rows * k_row_bytes : 0);
-        const int v_bytes = v_rows >= BN ? BN * v_row_bytes : (v_rows > 0 ? v_rows * v_row_bytes : 0);
-        const i32x4 rk = make_rsrc((const void*)k_next, k_bytes);
-        const i32x4 rv = make_rsrc((const void*)v_next, v_bytes);
-        i32x4 rkr = rk;
-        if constexpr (ROPE) {
-            rkr = make_rsrc((const void*)kr_next, k_rows >= BN ? BN * kr_row_bytes : (k_rows > 0 ? k_rows * kr_row_bytes : 0));
-            kr_next += BN * kr_row_bytes;
-        }
-        if constexpr (!PAGED) {
-            k_next += BN * k_row_bytes;
-            v_next += BN * v_row_bytes;
-        }
-        k_rows -= BN;
-        v_rows -= BN;
-
-        // causal / range mask on the tiles that cross a row's last visible key:
-        // key kt + c (c = mb*32 + (i>>2)*8 + lg*4 + (i&3)) is hidden when
-        // c > qlim - kt, with qlim = min(row position, ke - 1) - lg*4
-        if ((kt + BN - 1 > wave_first) || (kt + BN > ke)) {
-            const float ninf = -INFINITY;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-                const int lim = qlim[nb] - kt;
-#pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        // compare and select through VCC, one element at a time (no
-                        // batch of 64-bit lane masks in scalar registers)
-                        float x = s_cur[mb][nb][i];
-                        asm("v_cmp_gt_i32 vcc, %2, %1\n\tv_cndmask_b32 %0, %0, %3, vcc"
-                            : "+v"(x)
-                            : "v"(lim), "i"(mb * 32 + (i >> 2) * 8 + (i & 3)), "v"(ninf)
-                            : "vcc");
-                        s_cur[mb][nb][i] = x;
-                    }
-            }
-        }
-
-        float alpha[NB], m_use[NB], mx[NB][4], lsum[NB][2];  // mx: one partial max per max atom
-        bool refresh[NB];
+        // This lane's NB query rows (one per 32-column block of S^T), as B
+        // operands in AGPRs. Rows past the tile re-read its last row (their results
+        // are never stored), so every load stays inside q.
+        bf16x8 qf[NB][KS];
+        int qlim[NB];   // last key position the row may see, minus lg*4 (see masking)
+        bool qvalid[NB];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-            alpha[nb] = 1.f;
-            m_use[nb] = 0.f;
-            lsum[nb][0] = lsum[nb][1] = 0.f;
-            refresh[nb] = false;
+            const int rloc = wave * WROWS + nb * 32 + lr;
+            qvalid[nb] = rloc < it.nrows;
+            qlim[nb] = min(it.pos0 + rloc, ke - 1) - lg * 4;
+            const u16* qp = a.q + (int64_t)(it.row0 + min(rloc, it.nrows - 1)) * a.q_st + (int64_t)h * a.q_sh + lg * 8;
+            load_q_agpr<KS>(qf[nb], qp);
         }
-        float pprev = 0.f;
-        bf16x8 pb[NB][2][2];         // [nb][mb][hh]
-        bf16x8 kf[K_AHEAD + 1];      // K fragments in issue order, K_AHEAD in flight
-        bf16x8 vf[V_AHEAD + 1];      // V^T fragments in issue order, V_AHEAD in flight
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        const int wave_first = it.pos0 + wave * WROWS;
 
-        auto atom = [&](auto K) {
-            constexpr int k = decltype(K)::value;
-            if constexpr (k < A::MAXF) {
-                // max of 8 of the 32 scores of query block nb, as a depth-2 tree:
-                // the four atoms of a row are independent of each other
-                constexpr int nb = k >> 2, q = k & 3;
-                auto sc = [&](int j) -> float {
-                    const int v = q * 8 + j;  // score index in [mb*16 + i]
-                    return s_cur[v >> 4][nb][v & 15];
-                };
-                const float t0 = max3f(sc(0), sc(1), sc(2));
-                const float t1 = max3f(sc(3), sc(4), sc(5));
-                const float t2 = max2f(sc(6), sc(7));
-                mx[nb][q] = max3f(t0, t1, t2);
-            } else if constexpr (k < A::EXP) {
-                constexpr int nb = k - A::MAXF;
-                const float m =
-                    lane_swap32_max(max3f(mx[nb][0], mx[nb][1], max2f(mx[nb][2], mx[nb][3]))) * a.scale_log2;
-                // per-lane decision: the exps of this row wait only for VALU work;
-                // the wave-wide vote happens once, at the rescale check
-                refresh[nb] = m > m_run[nb] + LAZY_TAU;
-                const float m_new = refresh[nb] ? m : m_run[nb];
-                // a row that has seen no visible key yet (m_new = -inf) has nothing to rescale
-                alpha[nb] = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
-                m_run[nb] = m_new;
-                m_use[nb] = (m_new == -INFINITY) ? 0.f : m_new;
-                l_part[nb] *= alpha[nb];
-            } else {
-                constexpr int e = k - A::EXP;
-                constexpr int u = e >> 3, j = e & 7;
-                constexpr int mb = u / (2 * NB), hh = (u / NB) & 1, nb = u % NB;
-                const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mb][nb][hh * 8 + j], a.scale_log2, -m_use[nb]));
-                lsum[nb][j & 1] += pv;
-                if constexpr ((j & 1) == 0) {
-                    pprev = pv;
+        // Global->LDS copy of one tile through a buffer resource whose base is the
+        // tile's first key row and whose size ends at the last key of the range:
+        // rows past the range read as zeros (buffer range check), so the last tile
+        // needs no special case. Per-lane byte offsets are fixed for the kernel.
+        // Split key layout: the K tile is two LDS regions, the per-head part
+        // [BN][NOPE_GR] granules then the shared part [BN][ROPE_GR], each filled by
+        // its own copies (a copy instruction has one source) and swizzled for its
+        // own row width; the first NOPE_LOADS copies read k_nope, the rest k_rope.
+        constexpr int NOPE_LOADS = BN * NOPE_GR / NTHREADS;
+        constexpr int NOPE_BYTES = BN * NOPE_GR * 16;
+        uint32_t k_src[T::K_LOADS], v_src[T::V_LOADS];
+#pragma unroll
+        for (int t = 0; t < T::K_LOADS; ++t) {
+            if constexpr (ROPE) {
+                if (t < NOPE_LOADS) {
+                    const int slot = t * NTHREADS + tid;
+                    const int row = slot / NOPE_GR, gs = slot % NOPE_GR;
+                    k_src[t] = (uint32_t)(row * (int)a.k_st + kswz<NOPE_GR>(row, gs) * 8) * 2u;
                 } else {
-                    pb[nb][mb][hh][j - 1] = (__bf16)pprev;
-                    pb[nb][mb][hh][j] = (__bf16)pv;
+                    const int slot = (t - NOPE_LOADS) * NTHREADS + tid;
+                    const int row = slot / ROPE_GR, gs = slot % ROPE_GR;
+                    k_src[t] = (uint32_t)(row * (int)a.kr_st + kswz<ROPE_GR>(row, gs) * 8) * 2u;
                 }
+            } else {
+                const int slot = t * NTHREADS + tid;
+                const int row = slot / T::KGR, gs = slot % T::KGR;
+                k_src[t] = (uint32_t)(row * (int)a.k_st + kswz<T::KGR>(row, gs) * 8) * 2u;
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < T::V_LOADS; ++t) {
+            const int slot = t * NTHREADS + tid;
+            const int row = slot / T::VGR, gs = slot % T::VGR;
+            v_src[t] = (uint32_t)(row * (int)a.v_st + vswz<T::VGR>(row, gs) * 8) * 2u;
+        }
+        // resources over the rows [kt, min(kt + BN, ke)) (none when kt >= ke); the host
+        // keeps row strides below 2^31 / (2 BN) elements, so a tile's byte count fits
+        auto tile_bytes = [&](int kt, int32_t row_st) {
+            return (int32_t)((uint32_t)max(0, min(BN, ke - kt)) * (uint32_t)row_st * 2u);
+        };
+        auto k_rsrc = [&](int kt) { return make_rsrc(tile_src(kbase, a.k_sp, a.k_st, kt), tile_bytes(kt, a.k_st)); };
+        // the shared key part of the same rows (split layout; one row per key, no head)
+        const u16* rbase = ROPE ? a.k_rope + cache_row0 * a.kr_st : nullptr;
+        auto kr_rsrc = [&](int kt) { return make_rsrc(rbase + (int64_t)kt * a.kr_st, tile_bytes(kt, a.kr_st)); };
+        auto v_rsrc = [&](int kt) { return make_rsrc(tile_src(vbase, a.v_sp, a.v_st, kt), tile_bytes(kt, a.v_st)); };
+        const uint32_t lds_wave = (uint32_t)(uintptr_t)(lds_void_t*)smem + (uint32_t)wave * 1024u;
+        // copy t of the K (V) tile into buffer B: LDS offset from this wave's base
+        auto load_k = [&](const i32x4& r, const i32x4& rr, auto B, auto TT) {
+            constexpr int t = decltype(TT)::value;
+            if constexpr (ROPE && t >= NOPE_LOADS) {
+                constexpr int off = decltype(B)::value * T::K_BYTES + NOPE_BYTES + (t - NOPE_LOADS) * NWAVES * 1024;
+                copy16_to_lds<off>(rr, lds_wave, k_src[t]);
+            } else {
+                constexpr int off = decltype(B)::value * T::K_BYTES + t * NWAVES * 1024;
+                copy16_to_lds<off>(r, lds_wave, k_src[t]);
             }
         };
+        auto load_v = [&](const i32x4& r, auto B, auto TT) {
+            constexpr int off = 2 * T::K_BYTES + decltype(B)::value * T::V_BYTES + decltype(TT)::value * NWAVES * 1024;
+            copy16_to_lds<off>(r, lds_wave, v_src[decltype(TT)::value]);
+        };
+        auto issue_k = [&](auto B, int kt) {
+            const i32x4 r = k_rsrc(kt);
+            const i32x4 rr = ROPE ? kr_rsrc(kt) : r;
+            static_for<T::K_LOADS>([&](auto TT) { load_k(r, rr, B, TT); });
+        };
+        auto issue_v = [&](auto B, int kt) {
+            const i32x4 r = v_rsrc(kt);
+            static_for<T::V_LOADS>([&](auto TT) { load_v(r, B, TT); });
+        };
+        if (ntiles > 0) {
+            issue_k(std::integral_constant<int, 0>(), kt_first);
+            issue_v(std::integral_constant<int, 0>(), kt_first);
+            if (ntiles > 1) issue_k(std::integral_constant<int, 1>(), kt_first + dkt);
+        }
 
-        auto run = [&](auto tag) {
-            typedef typename decltype(tag)::type Sch;
-            constexpr Sch sch{};
-            constexpr int NS = Sch::NS;
-            typedef QkCoords<KS, NB> C;
-            // fragments needed first: V_AHEAD V^T fragments, and K_AHEAD K fragments of the next tile
-            static_for<V_AHEAD>([&](auto I) {
-                constexpr int f = I;
-                vf[f] = load_vfrag(vt_cur, (f / DB) >> 1, (f / DB) & 1, f % DB);
-            });
-            if constexpr (has_next)
-                static_for<K_AHEAD>([&](auto I) {
-                    constexpr int f = I;
-                    kf[f] = load_kfrag(kt_nxt, C::ks(NB * f), C::mb(NB * f));
-                });
-            static_for<NS>([&](auto SL) {
-                constexpr int s = SL;
-                constexpr int kind = sch.kind[s];
-                constexpr int idx = sch.index[s];
-                if constexpr (s == sch.rescale_before) {
-                    bool any = false;
+        // Per-lane LDS byte offsets; the rest of each address is an immediate.
+        // K (A operand of S^T): row mb*32+lr, logical granule ks*2+lg; row & 15 and
+        // (row >> 1) & 7 depend only on lr. The swizzle touches the low 4 (or 3)
+        // bits of the granule index, so K_OFFS offsets cover every ks and the
+        // higher granule bits are an immediate.
+        // (split key layout: K_OFFS offsets for the per-head region, KR_OFFS for the
+        // shared one)
+        constexpr int K_OFFS = ROPE ? NOPE_GR / 2 : ((T::KGR % 16 == 0) ? 8 : 4);
+        constexpr int KR_OFFS = ROPE ? ROPE_GR / 2 : 1;
+        int k_off[K_OFFS], kr_off[KR_OFFS];
 #pragma unroll
-                    for (int nb = 0; nb < NB; ++nb) any = any || refresh[nb];
-                    if (__builtin_amdgcn_ballot_w64(any) != 0) {
-                        // rare: rescale the AGPR accumulators 16 at a time, so the
-                        // branch needs only a few temporary VGPRs (alpha = 1 in the
-                        // lanes whose reference did not move)
-                        mfma_drain();
-                        static_for<NB * DB>([&](auto J) {
-                            constexpr int nb = J / DB, d = J % DB;
-                            scale_agpr_tile(o[d][nb], alpha[nb]);
-                            __builtin_amdgcn_sched_barrier(0);
-                        });
+        for (int r = 0; r < K_OFFS; ++r) {
+            if constexpr (ROPE) k_off[r] = lr * (NOPE_GR * 16) + kswz<NOPE_GR>(lr, r * 2 + lg) * 16;
+            else k_off[r] = lr * (T::KGR * 16) + kswz<T::KGR>(lr, r * 2 + lg) * 16;
+        }
+#pragma unroll
+        for (int r = 0; r < KR_OFFS; ++r) kr_off[r] = ROPE ? lr * (ROPE_GR * 16) + kswz<ROPE_GR>(lr, r * 2 + lg) * 16 : 0;
+        // V^T (A operand of O^T) through ds_read_b64_tr_b16: 16-lane group q reads
+        // keys 4*(q>>1) + (j>>2) and value columns 16*(q&1) + 4*(j&3) .. +3, i.e.
+        // granule 4*d + (tr_col >> 3) of value block d; key & 3 = tr_key & 3.
+        const int tq = lane >> 4, tj = lane & 15;
+        const int tr_key = 4 * (tq >> 1) + (tj >> 2);
+        const int tr_col = 16 * (tq & 1) + 4 * (tj & 3);
+        int v_off[DB];
+#pragma unroll
+        for (int d = 0; d < DB; ++d)
+            v_off[d] = tr_key * (T::VGR * 16) + vswz<T::VGR>(tr_key, d * 4 + (tr_col >> 3)) * 16 + (tr_col & 7) * 2;
+
+        float m_run[NB];   // max used by exp2 (log2 units), refreshed lazily
+        float l_part[NB];  // this lane's share of the softmax denominator
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            m_run[nb] = -INFINITY;
+            l_part[nb] = 0.f;
+        }
+        f32x16 o[DB][NB];
+#pragma unroll
+        for (int d = 0; d < DB; ++d)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) o[d][nb][i] = 0.f;
+
+        auto load_kfrag = [&](const char* kt_buf, int ks, int mb) -> bf16x8 {
+            if constexpr (ROPE) {
+                const char* addr = ks < NOPE_GR / 2
+                                       ? kt_buf + mb * 32 * NOPE_GR * 16 + k_off[ks]
+                                       : kt_buf + NOPE_BYTES + mb * 32 * ROPE_GR * 16 + kr_off[ks - NOPE_GR / 2];
+                return __builtin_bit_cast(bf16x8, *(const u32x4*)addr);
+            } else {
+                const u32x4 raw = *(const u32x4*)(kt_buf + mb * 32 * T::KGR * 16 + (ks / K_OFFS) * (K_OFFS * 32) +
+                                                  k_off[ks % K_OFFS]);
+                return __builtin_bit_cast(bf16x8, raw);
+            }
+        };
+        auto load_vfrag = [&](const char* vt, int mb, int hh, int d) -> bf16x8 {
+            bf16x8 af;
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const char* addr = vt + (mb * 32 + hh * 16 + half * 8) * T::VGR * 16 + v_off[d];
+                const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(addr));
+                const bf16x4 rb = __builtin_bit_cast(bf16x4, r);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) af[half * 4 + j] = rb[j];
+            }
+            return af;
+        };
+
+        // S^T = K Q^T for a whole tile (prologue only: no softmax to overlap with)
+        auto qk_all = [&](const char* kt_buf, f32x16 (&s)[2][NB]) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb) {
+                    const bf16x8 af = load_kfrag(kt_buf, ks, mb);
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb) {
+                        const bf16x8 bq = qf[nb][ks];
+                        if (ks == 0) MFMA_32x32x16_INIT(s[mb][nb], af, bq);
+                        else MFMA_32x32x16_ACC(s[mb][nb], af, bq);
                     }
                 }
-                if constexpr (has_next) {
-                    constexpr int NL = T::K_LOADS + T::V_LOADS;
-                    constexpr int LSTRIDE = (NS / LOAD_SPREAD) / NL > 0 ? (NS / LOAD_SPREAD) / NL : 1;
-                    if constexpr (s % LSTRIDE == 0 && s / LSTRIDE < NL) {
-                        constexpr int j = s / LSTRIDE;
-                        if constexpr (j < T::V_LOADS) {
-                            load_v(rv, std::integral_constant<int, 1 - par>(), std::integral_constant<int, j>());
-                        } else {
-                            load_k(rk, rkr, std::integral_constant<int, par>(),
-                                   std::integral_constant<int, j - T::V_LOADS>());
+        };
+
+        // Running sources of the copies a step issues (K of visit t+2, V of visit
+        // t+1): scalar pointer, first key and visits left, advanced by one tile per
+        // step. Past the last visit a copy gets an empty resource; its pointer may
+        // then run outside the tensor, but an empty resource never reads it.
+        const uint32_t k_row_bytes = (uint32_t)a.k_st * 2u, v_row_bytes = (uint32_t)a.v_st * 2u;
+        // V of visit t+1 is one visit behind K of visit t+2: its first key is
+        // kt_k - dkt and it has one visit more left
+        uint64_t k_next = PAGED ? 0 : (uint64_t)(uintptr_t)kbase + (uint64_t)((int64_t)(kt_first + 2 * dkt) * k_row_bytes);
+        uint64_t v_next = PAGED ? 0 : (uint64_t)(uintptr_t)vbase + (uint64_t)((int64_t)(kt_first + dkt) * v_row_bytes);
+        int kt_k = kt_first + 2 * dkt;
+        int k_left = ntiles - 2;
+        // split key layout: the shared part's running source (same rows as K)
+        const uint32_t kr_row_bytes = ROPE ? (uint32_t)a.kr_st * 2u : 0u;
+        uint64_t kr_next = ROPE ? (uint64_t)(uintptr_t)rbase + (uint64_t)((int64_t)(kt_first + 2 * dkt) * kr_row_bytes) : 0;
+        // one tile of rows in bytes (below 2^31), signed by the direction
+        auto tile_step = [&](uint32_t row_bytes) { return (uint64_t)(int64_t)(rev ? -(int32_t)(BN * row_bytes) : (int32_t)(BN * row_bytes)); };
+        // paged cache: the page of the K tile a step copies is read one step ahead
+        // (raw, clamped at its use), and V(t+1) shares K(t+1)'s page; table reads
+        // are clamped to the rows of the key range
+        auto clamp_row = [&](int row) { return min(max(row, kv_off + kb), last_row); };
+        int pg_pending = 0, pg_prev = 0;
+        if constexpr (PAGED) {
+            if (ntiles > 0) {
+                pg_prev = page_of(clamp_row(kv_off + kt_first + dkt));
+                pg_pending = bt_row[clamp_row(kv_off + kt_first + 2 * dkt) >> a.page_shift];
+            }
+        }
+
+        // One key tile: mask S(t) if needed, then the scheduled mix of S(t+1)
+        // MFMAs, the softmax of S(t) and the O^T += V^T P^T MFMAs of tile t.
+        auto step = [&](auto P, auto HAS_NEXT, int t, f32x16 (&s_cur)[2][NB], f32x16 (&s_nxt)[2][NB]) {
+            constexpr int par = decltype(P)::value;
+            constexpr bool has_next = decltype(HAS_NEXT)::value;
+            const char* kt_nxt = kbuf0 + (1 - par) * T::K_BYTES;
+            const char* vt_cur = vbuf0 + par * T::V_BYTES;
+            const int kt = kt_first + t * dkt;
+            wait_vmcnt<0>();
+            lds_barrier();  // K(t+1), V(t) are in LDS; every wave is done with K(t) and V(t-1)
+            // the next tiles' copies (K(t+2) into the K buffer just freed, V(t+1)
+            // into the V buffer just freed) are spread over the first slots. Past
+            // the last tile the resources are empty: the copies then only write
+            // zeros into buffers that no later step reads, and the step needs no
+            // branch around them.
+            if constexpr (PAGED) {
+                // the page read during the previous step is complete after the
+                // barrier; the empty asm pins its use here, before any LDS read of
+                // this step is in flight
+                int pg_k = clamp_page(__builtin_amdgcn_readfirstlane(pg_pending));
+                asm volatile("" : "+s"(pg_k) : : "memory");
+                const int row_k = kv_off + kt_k, row_v = row_k - dkt;
+                k_next = (uint64_t)(uintptr_t)(kbase + (int64_t)pg_k * a.k_sp + (int64_t)(row_k & pmask) * a.k_st);
+                v_next = (uint64_t)(uintptr_t)(vbase + (int64_t)pg_prev * a.v_sp + (int64_t)(row_v & pmask) * a.v_st);
+                pg_prev = pg_k;
+                pg_pending = bt_row[clamp_row(row_k + dkt) >> a.page_shift];
+            }
+            // rows of the copied tile (a tile is partial only at the end of the
+            // range), times the row bytes (below 2^31); none past the last visit
+            const uint32_t k_n = k_left > 0 ? (uint32_t)min(BN, ke - kt_k) : 0u;
+            const uint32_t v_n = k_left >= 0 ? (uint32_t)min(BN, ke - (kt_k - dkt)) : 0u;
+            const i32x4 rk = make_rsrc((const void*)k_next, (int32_t)(k_n * k_row_bytes));
+            const i32x4 rv = make_rsrc((const void*)v_next, (int32_t)(v_n * v_row_bytes));
+            i32x4 rkr = rk;
+            if constexpr (ROPE) {
+                rkr = make_rsrc((const void*)kr_next, (int32_t)(k_n * kr_row_bytes));
+                kr_next += tile_step(kr_row_bytes);
+            }
+            if constexpr (!PAGED) {
+                k_next += tile_step(k_row_bytes);
+                v_next += tile_step(v_row_bytes);
+            }
+            kt_k += dkt;
+            --k_left;
+
+            // causal / range mask on the tiles that cross a row's last visible key:
+            // key kt + c (c = mb*32 + (i>>2)*8 + lg*4 + (i&3)) is hidden when
+            // c > qlim - kt, with qlim = min(row position, ke - 1) - lg*4
+            if ((kt + BN - 1 > wave_first) || (kt + BN > ke)) {
+                const float ninf = -INFINITY;
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                    const int lim = qlim[nb] - kt;
+#pragma unroll
+                    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            // compare and select through VCC, one element at a time (no
+                            // batch of 64-bit lane masks in scalar registers)
+                            float x = s_cur[mb][nb][i];
+                            asm("v_cmp_gt_i32 vcc, %2, %1\n\tv_cndmask_b32 %0, %0, %3, vcc"
+                                : "+v"(x)
+                                : "v"(lim), "i"(mb * 32 + (i >> 2) * 8 + (i & 3)), "v"(ninf)
+                                : "vcc");
+                            s_cur[mb][nb][i] = x;
+                        }
+                }
+            }
+
+            float alpha[NB], m_use[NB], mx[NB][4], lsum[NB][2];  // mx: one partial max per max atom
+            bool refresh[NB];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+                alpha[nb] = 1.f;
+                m_use[nb] = 0.f;
+                lsum[nb][0] = lsum[nb][1] = 0.f;
+                refresh[nb] = false;
+            }
+            float pprev = 0.f;
+            bf16x8 pb[NB][2][2];         // [nb][mb][hh]
+            bf16x8 kf[K_AHEAD + 1];      // K fragments in issue order, K_AHEAD in flight
+            bf16x8 vf[V_AHEAD + 1];      // V^T fragments in issue order, V_AHEAD in flight
+
+            auto atom = [&](auto K) {
+                constexpr int k = decltype(K)::value;
+                if constexpr (k < A::MAXF) {
+                    // max of 8 of the 32 scores of query block nb, as a depth-2 tree:
+                    // the four atoms of a row are independent of each other
+                    constexpr int nb = k >> 2, q = k & 3;
+                    auto sc = [&](int j) -> float {
+                        const int v = q * 8 + j;  // score index in [mb*16 + i]
+                        return s_cur[v >> 4][nb][v & 15];
+                    };
+                    const float t0 = max3f(sc(0), sc(1), sc(2));
+                    const float t1 = max3f(sc(3), sc(4), sc(5));
+                    const float t2 = max2f(sc(6), sc(7));
+                    mx[nb][q] = max3f(t0, t1, t2);
+                } else if constexpr (k < A::EXP) {
+                    constexpr int nb = k - A::MAXF;
+                    const float m =
+                        lane_swap32_max(max3f(mx[nb][0], mx[nb][1], max2f(mx[nb][2], mx[nb][3]))) * a.scale_log2;
+                    // per-lane decision: the exps of this row wait only for VALU work;
+                    // the wave-wide vote happens once, at the rescale check
+                    refresh[nb] = m > m_run[nb] + LAZY_TAU;
+                    const float m_new = refresh[nb] ? m : m_run[nb];
+                    // a row that has seen no visible key yet (m_new = -inf) has nothing to rescale
+                    alpha[nb] = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[nb] - m_new);
+                    m_run[nb] = m_new;
+                    m_use[nb] = (m_new == -INFINITY) ? 0.f : m_new;
+                    l_part[nb] *= alpha[nb];
+                } else {
+                    constexpr int e = k - A::EXP;
+                    constexpr int u = e >> 3, j = e & 7;
+                    constexpr int mb = u / (2 * NB), hh = (u / NB) & 1, nb = u % NB;
+                    const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mb][nb][hh * 8 + j], a.scale_log2, -m_use[nb]));
+                    lsum[nb][j & 1] += pv;
+                    if constexpr ((j & 1) == 0) {
+                        pprev = pv;
+                    } else {
+                        pb[nb][mb][hh][j - 1] = (__bf16)pprev;
+                        pb[nb][mb][hh][j] = (__bf16)pv;
+                    }
+                }
+            };
+
+            auto run = [&](auto tag) {
+                typedef typename decltype(tag)::type Sch;
+                constexpr Sch sch{};
+                constexpr int NS = Sch::NS;
+                typedef QkCoords<KS, NB> C;
+                // fragments needed first: V_AHEAD V^T fragments, and K_AHEAD K fragments of the next tile
+                static_for<V_AHEAD>([&](auto I) {
+                    constexpr int f = I;
+                    vf[f] = load_vfrag(vt_cur, (f / DB) >> 1, (f / DB) & 1, f % DB);
+                });
+                if constexpr (has_next)
+                    static_for<K_AHEAD>([&](auto I) {
+                        constexpr int f = I;
+                        kf[f] = load_kfrag(kt_nxt, C::ks(NB * f), C::mb(NB * f));
+                    });
+                static_for<NS>([&](auto SL) {
+                    constexpr int s = SL;
+                    constexpr int kind = sch.kind[s];
+                    constexpr int idx = sch.index[s];
+                    if constexpr (s == sch.rescale_before) {
+                        bool any = false;
+#pragma unroll
+                        for (int nb = 0; nb < NB; ++nb) any = any || refresh[nb];
+                        if (__builtin_amdgcn_ballot_w64(any) != 0) {
+                            // rare: rescale the AGPR accumulators 16 at a time, so the
+                            // branch needs only a few temporary VGPRs (alpha = 1 in the
+                            // lanes whose reference did not move)
+                            mfma_drain();
+                            static_for<NB * DB>([&](auto J) {
+                                constexpr int nb = J / DB, d = J % DB;
+                                scale_agpr_tile(o[d][nb], alpha[nb]);
+                                __builtin_amdgcn_sched_barrier(0);
+                            });
                         }
                     }
-                }
-                if constexpr (kind == 2) {
-                    // VALU-only slot
-                } else if constexpr (kind == 0) {
-                    constexpr int ks = C::ks(idx), mb = C::mb(idx), nb = C::nb(idx);
-                    constexpr int frag = idx / NB;  // (mb, ks) in issue order
-                    // prefetch K_AHEAD fragments ahead with this fragment's first MFMA
-                    if constexpr (nb == 0 && frag + K_AHEAD < 2 * KS)
-                        kf[(frag + K_AHEAD) % (K_AHEAD + 1)] =
-                            load_kfrag(kt_nxt, C::ks(NB * (frag + K_AHEAD)), C::mb(NB * (frag + K_AHEAD)));
-                    const bf16x8 af = kf[frag % (K_AHEAD + 1)];
-                    const bf16x8 bq = qf[nb][ks];
-                    if constexpr (ks == 0) MFMA_32x32x16_INIT(s_nxt[mb][nb], af, bq);
-                    else MFMA_32x32x16_ACC(s_nxt[mb][nb], af, bq);
-                } else {
-                    constexpr int grp = idx / (NB * DB), d = (idx / NB) % DB, nb = idx % NB;
-                    constexpr int mb = grp >> 1, hh = grp & 1;
-                    constexpr int frag = idx / NB;  // (grp, d) in issue order
-                    // prefetch V_AHEAD fragments ahead with this fragment's first MFMA
-                    if constexpr (nb == 0 && frag + V_AHEAD < 4 * DB) {
-                        constexpr int f2 = frag + V_AHEAD;
-                        vf[f2 % (V_AHEAD + 1)] = load_vfrag(vt_cur, (f2 / DB) >> 1, (f2 / DB) & 1, f2 % DB);
+                    if constexpr (has_next) {
+                        constexpr int NL = T::K_LOADS + T::V_LOADS;
+                        constexpr int LSTRIDE = (NS / LOAD_SPREAD) / NL > 0 ? (NS / LOAD_SPREAD) / NL : 1;
+                        if constexpr (s % LSTRIDE == 0 && s / LSTRIDE < NL) {
+                            constexpr int j = s / LSTRIDE;
+                            if constexpr (j < T::V_LOADS) {
+                                load_v(rv, std::integral_constant<int, 1 - par>(), std::integral_constant<int, j>());
+                            } else {
+                                load_k(rk, rkr, std::integral_constant<int, par>(),
+                                       std::integral_constant<int, j - T::V_LOADS>());
+                            }
+                        }
                     }
-                    o[d][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[frag % (V_AHEAD + 1)], pb[nb][mb][hh],
-                                                                       o[d][nb], 0, 0, 0);
-                }
-                constexpr int a0 = s == 0 ? 0 : sch.atoms_end[s == 0 ? 0 : s - 1];
-                constexpr int a1 = sch.atoms_end[s];
-                static_range<a0, a1>([&](auto K) { atom(K); });
-                __builtin_amdgcn_sched_barrier(0);
-            });
+                    if constexpr (kind == 2) {
+                        // VALU-only slot
+                    } else if constexpr (kind == 0) {
+                        constexpr int ks = C::ks(idx), mb = C::mb(idx), nb = C::nb(idx);
+                        constexpr int frag = idx / NB;  // (mb, ks) in issue order
+                        // prefetch K_AHEAD fragments ahead with this fragment's first MFMA
+                        if constexpr (nb == 0 && frag + K_AHEAD < 2 * KS)
+                            kf[(frag + K_AHEAD) % (K_AHEAD + 1)] =
+                                load_kfrag(kt_nxt, C::ks(NB * (frag + K_AHEAD)), C::mb(NB * (frag + K_AHEAD)));
+                        const bf16x8 af = kf[frag % (K_AHEAD + 1)];
+                        const bf16x8 bq = qf[nb][ks];
+                        if constexpr (ks == 0) MFMA_32x32x16_INIT(s_nxt[mb][nb], af, bq);
+                        else MFMA_32x32x16_ACC(s_nxt[mb][nb], af, bq);
+                    } else {
+                        constexpr int grp = idx / (NB * DB), d = (idx / NB) % DB, nb = idx % NB;
+                        constexpr int mb = grp >> 1, hh = grp & 1;
+                        constexpr int frag = idx / NB;  // (grp, d) in issue order
+                        // prefetch V_AHEAD fragments ahead with this fragment's first MFMA
+                        if constexpr (nb == 0 && frag + V_AHEAD < 4 * DB) {
+                            constexpr int f2 = frag + V_AHEAD;
+                            vf[f2 % (V_AHEAD + 1)] = load_vfrag(vt_cur, (f2 / DB) >> 1, (f2 / DB) & 1, f2 % DB);
+                        }
+                        o[d][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[frag % (V_AHEAD + 1)], pb[nb][mb][hh],
+                                                                           o[d][nb], 0, 0, 0);
+                    }
+                    constexpr int a0 = s == 0 ? 0 : sch.atoms_end[s == 0 ? 0 : s - 1];
+                    constexpr int a1 = sch.atoms_end[s];
+                    static_range<a0, a1>([&](auto K) { atom(K); });
+                    __builtin_amdgcn_sched_barrier(0);
+                });
+            };
+            if constexpr (has_next) run(std::type_identity<SchedFull>());
+            else run(std::type_identity<SchedLast>());
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) l_part[nb] += lsum[nb][0] + lsum[nb][1];
         };
-        if constexpr (has_next) run(std::type_identity<SchedFull>());
-        else run(std::type_identity<SchedLast>());
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) l_part[nb] += lsum[nb][0] + lsum[nb][1];
-    };
 
-    if (ntiles > 0) {
-        typedef std::integral_constant<int, 0> P0;
-        typedef std::integral_constant<int, 1> P1;
-        typedef std::integral_constant<bool, true> NX;
-        typedef std::integral_constant<bool, false> LAST;
-        f32x16 s_a[2][NB], s_b[2][NB];
-        wait_vmcnt<0>();
-        lds_barrier();
-        qk_all(kbuf0, s_a);
-        mfma_drain();
-        // Tiles in pairs (static buffer parity). With an even tile count the
-        // last pair computes one S^T tile too many, from stale LDS data, and
-        // discards it: cheaper than a third step variant's registers.
-        int t = 0;
-        for (; t + 1 < ntiles; t += 2) {
-            step(P0(), NX(), t, s_a, s_b);
-            step(P1(), NX(), t + 1, s_b, s_a);
+        if (ntiles > 0) {
+            typedef std::integral_constant<int, 0> P0;
+            typedef std::integral_constant<int, 1> P1;
+            typedef std::integral_constant<bool, true> NX;
+            typedef std::integral_constant<bool, false> LAST;
+            f32x16 s_a[2][NB], s_b[2][NB];
+            wait_vmcnt<0>();
+            lds_barrier();
+            qk_all(kbuf0, s_a);
+            mfma_drain();
+            // Tiles in pairs (static buffer parity). With an even tile count the
+            // last pair computes one S^T tile too many, from stale LDS data, and
+            // discards it: cheaper than a third step variant's registers.
+            int t = 0;
+            for (; t + 1 < ntiles; t += 2) {
+                step(P0(), NX(), t, s_a, s_b);
+                step(P1(), NX(), t + 1, s_b, s_a);
+            }
+            if (t < ntiles) step(P0(), LAST(), t, s_a, s_b);
+            mfma_drain();
+            // a pair's second step may still be copying (zeros) into LDS: no copy
+            // may outlive the workgroup's LDS allocation
+            wait_vmcnt<0>();
         }
-        if (t < ntiles) step(P0(), LAST(), t, s_a, s_b);
-        mfma_drain();
-        // a pair's second step may still be copying (zeros) into LDS: no copy
-        // may outlive the workgroup's LDS allocation
-        wait_vmcnt<0>();
-    }
 
-    // ---- epilogue: normalise and store ----
-    // The arguments only the epilogue needs are read again from the kernel
-    // argument segment (the empty asm hides that they were read before), so
-    // they do not occupy scalar registers across the key loop.
-    const AttnArgs* ka = (const AttnArgs*)__builtin_amdgcn_kernarg_segment_ptr();
-    asm volatile("" : "+s"(ka));
-    const WorkItem it2 = ka->items[item_id];
-    const int row0 = __builtin_amdgcn_readfirstlane(it2.row0);
-    const int split = __builtin_amdgcn_readfirstlane(it2.split);
+        // ---- epilogue: normalise and store ----
+        // The arguments only the epilogue needs are read again from the kernel
+        // argument segment (the empty asm hides that they were read before), so
+        // they do not occupy scalar registers across the key loop.
+        const AttnArgs* ka = (const AttnArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+        asm volatile("" : "+s"(ka));
+        const WorkItem it2 = ka->items[item_id];
+        const int row0 = __builtin_amdgcn_readfirstlane(it2.row0);
+        const int split = __builtin_amdgcn_readfirstlane(it2.split);
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const float l_tot = lane_swap32_add(l_part[nb]);
-        const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        const float lse_val = l_tot > 0.f ? (m_run[nb] + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
-        if (!qvalid[nb]) continue;
-        const int row = row0 + wave * WROWS + nb * 32 + lr;
-        if constexpr (SPLIT) {
-            float* po = (float*)ka->out + (((int64_t)split * ka->tokens + row) * ka->num_heads + h) * DV;
+        for (int nb = 0; nb < NB; ++nb) {
+            const float l_tot = lane_swap32_add(l_part[nb]);
+            const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            const float lse_val = l_tot > 0.f ? (m_run[nb] + __log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
+            if (!qvalid[nb]) continue;
+            const int row = row0 + wave * WROWS + nb * 32 + lr;
+            if constexpr (SPLIT) {
+                float* po = (float*)ka->out + (((int64_t)split * ka->tokens + row) * ka->num_heads + h) * DV;
 #pragma unroll
-            for (int d = 0; d < DB; ++d)
+                for (int d = 0; d < DB; ++d)
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    float4 w = {o[d][nb][c * 4 + 0] * inv_l, o[d][nb][c * 4 + 1] * inv_l,
-                                o[d][nb][c * 4 + 2] * inv_l, o[d][nb][c * 4 + 3] * inv_l};
-                    *(float4*)(po + d * 32 + c * 8 + lg * 4) = w;
-                }
-            if (lg == 0) ka->lse[((int64_t)split * ka->num_heads + h) * ka->tokens + row] = lse_val;
-        } else {
-            u16* op = (u16*)ka->out + (int64_t)row * ka->o_st + (int64_t)h * ka->o_sh;
+                    for (int c = 0; c < 4; ++c) {
+                        float4 w = {o[d][nb][c * 4 + 0] * inv_l, o[d][nb][c * 4 + 1] * inv_l,
+                                    o[d][nb][c * 4 + 2] * inv_l, o[d][nb][c * 4 + 3] * inv_l};
+                        *(float4*)(po + d * 32 + c * 8 + lg * 4) = w;
+                    }
+                if (lg == 0) ka->lse[((int64_t)split * ka->num_heads + h) * ka->tokens + row] = lse_val;
+            } else {
+                u16* op = (u16*)ka->out + (int64_t)row * ka->o_st + (int64_t)h * ka->o_sh;
 #pragma unroll
-            for (int d = 0; d < DB; ++d)
+                for (int d = 0; d < DB; ++d)
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    bf16x4 w;
+                    for (int c = 0; c < 4; ++c) {
+                        bf16x4 w;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][nb][c * 4 + j] * inv_l);
-                    *(bf16x4*)(op + d * 32 + c * 8 + lg * 4) = w;
-                }
-            if (lg == 0 && ka->lse) ka->lse[(int64_t)h * ka->lse_sh + row] = lse_val;
+                        for (int j = 0; j < 4; ++j) w[j] = (__bf16)(o[d][nb][c * 4 + j] * inv_l);
+                        *(bf16x4*)(op + d * 32 + c * 8 + lg * 4) = w;
+                    }
+                if (lg == 0 && ka->lse) ka->lse[(int64_t)h * ka->lse_sh + row] = lse_val;
+            }
         }
-    }
+    }  // slot entries
 }
 
 
@@ -1079,7 +1105,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
 
 template <int DQK, int DV, int NB, int KVM>
 hipError_t launch(const AttnArgs& a, bool split, const CombineArgs& ca, hipStream_t stream) {
-    const int64_t total = (int64_t)a.num_items * a.num_heads;
+    const int64_t total = (int64_t)a.num_slots * a.num_heads;
     if (total <= 0) return hipSuccess;
     if (total > (int64_t)INT32_MAX) return hipErrorInvalidValue;
     dim3 grid((unsigned)total), block(NTHREADS);
@@ -1186,6 +1212,7 @@ struct vpp_chunk_attn_plan_s {
     float scale;
     std::vector<WorkItem> items;
     std::vector<int32_t> item_seg;  // segment of each work item (paged runs)
+    int32_t num_slots = 0;          // workgroups per head: items.size() / 2
     int32_t num_tiles = 0;
     int32_t num_splits = 1;
     int32_t nb = 2;  // 32-row query blocks per wave of the kernel variant the plan was made for
@@ -1233,18 +1260,27 @@ vpp_status_t check_config(const vpp_chunk_attn_config_t& c) {
     return VPP_OK;
 }
 
-// Split count: explicit, or automatic -- split only when the chunk gives too
-// few workgroups to fill the chip and the key ranges are long enough that each
-// piece still streams many key tiles.
-int choose_splits(const vpp_chunk_attn_config_t& c, int tiles, double mean_key_tiles) {
-    if (c.num_splits >= 1) return c.num_splits;
-    const double wgs = (double)tiles * c.num_q_heads;
-    const double target = 2.0 * 256.0;
+// Split count. A split cuts the prefix [0, p) of a segment into n tile-aligned
+// parts common to all of its tiles; the last part runs on to each tile's own end
+// (its keys within the chunk), so pieces of one index read the same keys in every
+// tile. Explicit: the requested count, at most one piece per key tile of the
+// longest prefix (a chunk without a prefix is not split). Automatic: only when
+// the chunk gives too few workgroups to fill the chip, in pieces of at least
+// MIN_PIECE prefix keys.
+constexpr int64_t MIN_PIECE = 1024;
+int choose_splits(const vpp_chunk_attn_config_t& c, int64_t slots, int64_t max_prefix) {
+    if (c.num_splits >= 1)
+        return (int)std::min<int64_t>(c.num_splits, std::max<int64_t>(1, max_prefix / BN));
+    // a slot's two tiles balance each other, so one slot workgroup per CU fills the chip
+    const double wgs = (double)slots * c.num_q_heads;
+    const double target = 256.0;
     if (wgs >= target) return 1;
-    int n = (int)ceil(target / std::max(1.0, wgs));
-    n = std::min(n, (int)(mean_key_tiles / 8.0));
-    return std::max(1, std::min(n, MAX_SPLITS));
+    const int64_t n = (int64_t)ceil(target / std::max(1.0, wgs));
+    return (int)std::max<int64_t>(1, std::min<int64_t>({n, max_prefix / MIN_PIECE, (int64_t)MAX_SPLITS}));
 }
+
+// Boundary b of the n-part split of a p-key prefix (tile-aligned, b = 0 .. n-1).
+int32_t piece_begin(int64_t p, int n, int b) { return (int32_t)(((p / BN) * b / n) * BN); }
 
 }  // namespace
 
@@ -1286,11 +1322,25 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
         }
     const int nb = choose_nb(c, tiles256, tiles256 ? keys256 / tiles256 : 0.0);
     const int BM = block_rows(nb);
-    std::vector<WorkItem> tiles;
-    std::vector<int32_t> tile_seg;
-    double pairs = 0.0, key_tiles = 0.0;
+    // Work slots. A workgroup runs one slot: up to two query tiles of one segment,
+    // tile i with its key range ascending, then tile T-1-i (the partner from the
+    // other end of the segment) descending. A pair's two ranges together span the
+    // same number of keys in every slot of the segment, so the workgroups of a
+    // segment finish together; and at any moment they all read one of two key
+    // positions (the ascending front, and the descending one, which mirrors it), so
+    // the tiles running side by side on one XCD share each K/V tile through its L2.
+    // Slots are grouped by (segment, split piece); groups run longest first.
+    std::vector<WorkItem> items;
+    std::vector<int32_t> iseg;
+    double pairs = 0.0;
+    int ntiles = 0, nsplit = 1;
     try {
+        struct Seg { int t0, t1; };  // the segment's tiles in `tiles`
+        std::vector<WorkItem> tiles;
+        std::vector<Seg> segs((size_t)num_segments);
+        int64_t slots = 0, max_prefix = 0;
         for (int s = 0; s < num_segments; ++s) {
+            segs[s].t0 = (int)tiles.size();
             for (int r0 = cu_q[s]; r0 < cu_q[s + 1]; r0 += BM) {
                 WorkItem w;
                 w.row0 = r0;
@@ -1301,53 +1351,54 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
                 w.split = 0;
                 w.kv_base = kv_start[s];
                 tiles.push_back(w);
-                tile_seg.push_back(s);
                 // visible pairs: sum over rows of (position + 1)
                 pairs += (double)w.nrows * (double)w.pos0 + 0.5 * (double)w.nrows * (w.nrows + 1);
-                key_tiles += ceil((double)w.key_end / BN);
             }
+            segs[s].t1 = (int)tiles.size();
+            slots += (segs[s].t1 - segs[s].t0 + 1) / 2;
+            if (segs[s].t1 > segs[s].t0) max_prefix = std::max(max_prefix, prefix_len[s]);
         }
-    } catch (const std::bad_alloc&) {
-        return VPP_ERR_NOMEM;
-    }
-    const int ntiles = (int)tiles.size();
-    const int nsplit = ntiles ? choose_splits(c, ntiles, key_tiles / ntiles) : 1;
+        ntiles = (int)tiles.size();
+        nsplit = ntiles ? choose_splits(c, slots, max_prefix) : 1;
 
-    std::vector<WorkItem> items;
-    std::vector<int32_t> iseg;
-    try {
-        items.reserve((size_t)ntiles * nsplit);
-        iseg.reserve((size_t)ntiles * nsplit);
-        for (size_t ti = 0; ti < tiles.size(); ++ti) {
-            const WorkItem& t = tiles[ti];
-            const int nkt = (t.key_end + BN - 1) / BN;
-            for (int sp = 0; sp < nsplit; ++sp) {
-                WorkItem w = t;
-                w.split = sp;
-                if (nsplit > 1) {
-                    w.key_begin = (int32_t)((int64_t)nkt * sp / nsplit) * BN;
-                    w.key_end = sp + 1 == nsplit ? t.key_end : (int32_t)((int64_t)nkt * (sp + 1) / nsplit) * BN;
-                    w.key_end = std::min(w.key_end, t.key_end);
-                    w.key_begin = std::min(w.key_begin, w.key_end);
+        struct Group { int seg, piece; int64_t len; size_t first, count; };  // slots [first, first+count)
+        std::vector<Group> groups;
+        std::vector<WorkItem> grouped;  // two items per slot, group by group
+        const WorkItem none = {0, 0, 0, 0, 0, 0, 0};
+        for (int s = 0; s < num_segments; ++s) {
+            const int T = segs[s].t1 - segs[s].t0;
+            if (T == 0) continue;
+            for (int b = 0; b < nsplit; ++b) {
+                auto piece = [&](int ti) {
+                    WorkItem w = tiles[segs[s].t0 + ti];
+                    w.split = b;
+                    if (nsplit > 1) {
+                        w.key_begin = piece_begin(prefix_len[s], nsplit, b);
+                        if (b + 1 < nsplit) w.key_end = piece_begin(prefix_len[s], nsplit, b + 1);
+                    }
+                    return w;
+                };
+                Group g{s, b, 0, grouped.size() / 2, 0};
+                for (int i = 0; i < (T + 1) / 2; ++i) {
+                    const WorkItem x = piece(i);
+                    const WorkItem y = (T - 1 - i != i) ? piece(T - 1 - i) : none;
+                    grouped.push_back(x);
+                    grouped.push_back(y);
+                    const int64_t len = (int64_t)(x.key_end - x.key_begin) + (y.nrows ? y.key_end - y.key_begin : 0);
+                    g.len = std::max(g.len, len);
+                    ++g.count;
                 }
-                items.push_back(w);
-                iseg.push_back(tile_seg[ti]);
+                groups.push_back(g);
             }
         }
-        // longest key range first, so the short ones fill the tail of the launch
-        std::vector<int32_t> order(items.size());
-        for (size_t i = 0; i < order.size(); ++i) order[i] = (int32_t)i;
-        std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
-            return (items[x].key_end - items[x].key_begin) > (items[y].key_end - items[y].key_begin);
-        });
-        std::vector<WorkItem> sorted(items.size());
-        std::vector<int32_t> sorted_seg(items.size());
-        for (size_t i = 0; i < order.size(); ++i) {
-            sorted[i] = items[order[i]];
-            sorted_seg[i] = iseg[order[i]];
-        }
-        items.swap(sorted);
-        iseg.swap(sorted_seg);
+        std::stable_sort(groups.begin(), groups.end(), [](const Group& x, const Group& y) { return x.len > y.len; });
+        items.reserve(grouped.size());
+        iseg.reserve(grouped.size());
+        for (const Group& g : groups)
+            for (size_t k = 0; k < 2 * g.count; ++k) {
+                items.push_back(grouped[2 * g.first + k]);
+                iseg.push_back(g.seg);
+            }
     } catch (const std::bad_alloc&) {
         return VPP_ERR_NOMEM;
     }
@@ -1366,6 +1417,7 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
     p->num_splits = nsplit;
     p->tokens = cu_q[num_segments];
     p->pairs = pairs;
+    p->num_slots = (int32_t)(p->items.size() / 2);
     p->items_bytes = p->items.size() * sizeof(WorkItem);
     size_t ws = align256(std::max<size_t>(p->items_bytes, 1));
     if (nsplit > 1) {
@@ -1382,6 +1434,7 @@ extern "C" vpp_status_t vpp_chunk_attn_plan_info(vpp_chunk_attn_plan_t p, vpp_ch
     info->num_tiles = p->num_tiles;
     info->num_splits = p->num_splits;
     info->num_work_items = (int32_t)p->items.size();
+    info->num_slots = p->num_slots;
     info->block_m = block_rows(p->nb);
     info->block_n = BN;
     info->num_tokens = p->tokens;
@@ -1464,16 +1517,18 @@ vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int6
         !stride_ok(v_sh) || !stride_ok(o_st) || !stride_ok(o_sh))
         return VPP_ERR_INVALID_ARG;
     if (lse && (((uintptr_t)lse & 3u) != 0 || lse_sh < p->tokens)) return VPP_ERR_INVALID_ARG;
-    // the kernels keep element strides in 32 bits; a stride times the 64 rows of
-    // a tile must also stay below 2^31 for the buffer resources
+    // the kernels keep element strides in 32 bits; the bytes of one key tile
+    // (BN rows of a cache row stride, 2 bytes an element) must also stay below
+    // 2^31, the range of a buffer resource's size field
     const int64_t smax = ((int64_t)1 << 31) / 64;
-    if (q_st >= smax || q_sh >= smax || k_st >= smax || k_sh >= smax || v_st >= smax || v_sh >= smax ||
-        o_st >= smax || o_sh >= smax || (lse && lse_sh >= ((int64_t)1 << 31)))
+    const int64_t row_smax = ((int64_t)1 << 31) / (2 * BN);
+    if (q_st >= smax || q_sh >= smax || k_st >= row_smax || k_sh >= smax || v_st >= row_smax ||
+        v_sh >= smax || o_st >= smax || o_sh >= smax || (lse && lse_sh >= ((int64_t)1 << 31)))
         return VPP_ERR_INVALID_ARG;
     if (rope) {
         if (p->cfg.head_dim_qk != 192 || p->cfg.head_dim_v != 128) return VPP_ERR_UNSUPPORTED;
         if (!rope->k_rope || !aligned16(rope->k_rope) || !stride_ok(rope->kr_st) || rope->kr_st < 64 ||
-            rope->kr_st >= smax)
+            rope->kr_st >= row_smax)
             return VPP_ERR_INVALID_ARG;
     }
     if (!workspace || ((uintptr_t)workspace & 255u) != 0) return VPP_ERR_WORKSPACE;
@@ -1523,7 +1578,9 @@ vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int6
     a.q_st = (int32_t)q_st; a.q_sh = (int32_t)q_sh; a.k_st = (int32_t)k_st; a.k_sh = (int32_t)k_sh;
     a.v_st = (int32_t)v_st; a.v_sh = (int32_t)v_sh; a.o_st = (int32_t)o_st; a.o_sh = (int32_t)o_sh;
     a.lse_sh = (int32_t)lse_sh;
-    a.num_items = (int32_t)p->items.size();
+    // one workgroup per slot and head: the kernel reads entries 2*slot and 2*slot + 1
+    a.num_slots = p->num_slots;
+    a.num_entries = (int32_t)p->items.size();
     a.num_heads = c.num_q_heads;
     a.group = c.num_q_heads / c.num_kv_heads;
     a.tokens = p->tokens;

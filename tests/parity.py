@@ -129,3 +129,11 @@ def run_chunk(attn, q, k_cache, v_cache, cu_q, kv_start, prefix_len, lse_cols: i
     attn.run(q[:tok], k_cache, v_cache, out, lse)
     torch.cuda.synchronize()
     return out, lse
+
+
+def planned_splits(requested, prefixes, lens, tile=64):
+    """Split count a plan uses for a fixed request: the request, capped at one key
+    tile of prefix per piece (longest prefix of a segment with rows); a chunk with
+    no prefix is not split."""
+    longest = max([int(p) for p, n in zip(prefixes, lens) if int(n) > 0], default=0)
+    return min(int(requested), max(1, longest // tile))

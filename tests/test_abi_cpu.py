@@ -107,35 +107,68 @@ def check_plan(c, cu, ks, pl):
     finally:
         B.vpp_chunk_attn_destroy(h)
     bm, bn, n = info.block_m, info.block_n, info.num_splits
-    assert info.num_work_items == len(items) == info.num_tiles * n
+    # two entries per work slot (one workgroup per slot and head); a second entry
+    # without rows is empty
+    assert info.num_work_items == len(items) and len(items) % 2 == 0
+    # the launch runs one workgroup per slot and head
+    assert info.num_slots * 2 == len(items)
     assert ws == info.workspace_bytes and ws >= len(items) * 32
-    # longest key range first
-    lens = items["key_end"] - items["key_begin"]
-    assert np.all(np.diff(lens) <= 0)
+    slots = items.reshape(-1, 2)
+    assert np.all(slots[:, 0]["nrows"] >= 1)
+    seg_of = lambda row0: int(np.searchsorted(cu, row0, side="right") - 1)  # noqa: E731
     # tiles: rows partition the chunk, positions and bases follow the segments
     tiles = {}
-    for it in items:
+    for it in items[items["nrows"] > 0]:
         tiles.setdefault(int(it["row0"]), []).append(it)
+    assert info.num_tiles == len(tiles)
     covered = np.zeros(int(cu[-1]), dtype=np.int32)
     pairs = 0
+    bounds = {}
     for row0, its in tiles.items():
         assert len(its) == n
         t = its[0]
         assert 1 <= t["nrows"] <= bm
         covered[row0:row0 + t["nrows"]] += 1
-        s = int(np.searchsorted(cu, row0, side="right") - 1)
+        s = seg_of(row0)
         assert row0 + t["nrows"] <= cu[s + 1], "a tile crosses a segment boundary"
         assert t["pos0"] == pl[s] + row0 - cu[s]
         assert t["kv_base"] == ks[s]
-        # splits cover [0, last position + 1) exactly, in order, tile-aligned inside
+        # pieces cover [0, last position + 1) exactly, in order, tile-aligned inside;
+        # every piece below the last ends inside the prefix, at a boundary common to
+        # all tiles of the segment
         rng = sorted((int(x["split"]), int(x["key_begin"]), int(x["key_end"])) for x in its)
         assert [r[0] for r in rng] == list(range(n))
         assert rng[0][1] == 0 and rng[-1][2] == t["pos0"] + t["nrows"]
         for a, b in zip(rng, rng[1:]):
-            assert a[2] == b[1] and a[2] % bn == 0
+            assert a[2] == b[1] and a[2] % bn == 0 and a[2] <= pl[s]
+        assert bounds.setdefault(s, [r[1] for r in rng]) == [r[1] for r in rng]
         pairs += int(t["nrows"]) * int(t["pos0"]) + int(t["nrows"]) * (int(t["nrows"]) + 1) // 2
     assert np.all(covered == 1)
     assert info.pairs == pairs
+    # a slot pairs a tile with its partner from the other end of the same segment,
+    # in the same piece; the pair's key counts add up alike within a (segment,
+    # piece) group, and groups run longest first
+    groups = {}
+    order = []
+    for a, b in slots:
+        s = seg_of(int(a["row0"]))
+        ln = int(a["key_end"] - a["key_begin"])
+        if b["nrows"]:
+            assert seg_of(int(b["row0"])) == s and b["split"] == a["split"] and b["row0"] > a["row0"]
+            ln += int(b["key_end"] - b["key_begin"])
+        key = (s, int(a["split"]))
+        if key not in groups:
+            order.append(key)
+        groups.setdefault(key, []).append((ln, bool(b["nrows"])))
+    for key, lens in groups.items():
+        full = [x for x, two in lens if two]
+        if full:
+            assert max(full) - min(full) <= bm, (key, lens)
+        # the groups' slots are contiguous
+    seen = [(seg_of(int(a["row0"])), int(a["split"])) for a, _ in slots]
+    assert [k for i, k in enumerate(seen) if i == 0 or seen[i - 1] != k] == order, "a group is not contiguous"
+    glen = [max(x for x, _ in groups[k]) for k in order]
+    assert all(x >= y for x, y in zip(glen, glen[1:]))
     return info
 
 
@@ -148,7 +181,8 @@ def test_plan_workload_chunks(name):
         _, cu, ks, pl = W.chunk_segments(w, k)
         info = check_plan(c, cu, ks, pl)
         if w.num_splits > 0:
-            assert info.num_splits == w.num_splits
+            # a fixed count applies once the prefix has a key tile per piece
+            assert info.num_splits == min(w.num_splits, max(1, int(pl[0]) // 64))
 
 
 def test_plan_mixed_chunks():
@@ -206,6 +240,46 @@ def test_run_argument_checks_before_any_device_work():
         assert call(wsb=ws - 1) == B.VPP_ERR_WORKSPACE
         assert lib.vpp_chunk_attn_run(None, good, 1024, 128, good, 256, 128, good, 256, 128,
                                       good, 1024, 128, 0, 0, good, ws, None) == B.VPP_ERR_INVALID_ARG
+    finally:
+        B.vpp_chunk_attn_destroy(h)
+
+
+def test_cache_row_stride_boundary():
+    """A key tile (64 rows of the cache row stride, 2 bytes an element) must span less
+    than 2^31 bytes: row strides up to 2^24 - 8 elements pass the argument checks,
+    2^24 is refused. The workspace is one byte short, so a stride that passes stops
+    at the workspace check and no device work is ever enqueued."""
+    lib = B.load()
+    h, ws = B.vpp_chunk_attn_plan(cfg(), [0, 64], [0], [0])
+    try:
+        good = 1 << 20
+        ok, bad = (1 << 24) - 8, 1 << 24
+
+        def call(k_st=256, v_st=256, q_st=1024):
+            return lib.vpp_chunk_attn_run(h, good, q_st, 128, good, k_st, 128, good, v_st, 128,
+                                          good, 1024, 128, 0, 0, good, ws - 1, None)
+        assert call(k_st=ok) == B.VPP_ERR_WORKSPACE
+        assert call(v_st=ok) == B.VPP_ERR_WORKSPACE
+        assert call(k_st=bad) == B.VPP_ERR_INVALID_ARG
+        assert call(v_st=bad) == B.VPP_ERR_INVALID_ARG
+        # query strides are not tile-bounded: only the 32-bit element-stride limit applies
+        assert call(q_st=bad) == B.VPP_ERR_WORKSPACE
+        assert call(q_st=1 << 25) == B.VPP_ERR_INVALID_ARG
+    finally:
+        B.vpp_chunk_attn_destroy(h)
+
+
+def test_split_key_row_stride_boundary():
+    lib = B.load()
+    h, ws = B.vpp_chunk_attn_plan(cfg(hq=2, hkv=2, dqk=192, dv=128), [0, 64], [0], [0])
+    try:
+        good = 1 << 20
+
+        def call(kr_st):
+            return lib.vpp_chunk_attn_run_mla(h, good, 384, 192, good, 256, 128, good, kr_st, good, 256, 128,
+                                              good, 256, 128, None, 0, good, ws - 1, None)
+        assert call((1 << 24) - 8) == B.VPP_ERR_WORKSPACE
+        assert call(1 << 24) == B.VPP_ERR_INVALID_ARG
     finally:
         B.vpp_chunk_attn_destroy(h)
 
@@ -268,4 +342,7 @@ def test_plan_random_segment_mixes(mix):
     c = cfg(hq=hq, hkv=hkv, dqk=dqk, dv=dv, max_tok=int(cu[-1]), max_kv=max(rows, 1), splits=splits)
     info = check_plan(c, cu, starts, prefixes)
     if splits > 0:
-        assert info.num_splits == splits
+        # a fixed count, capped at one key tile of prefix per piece (longest prefix
+        # of a segment with rows)
+        longest = max([p for p, n in zip(prefixes, lens) if n > 0], default=0)
+        assert info.num_splits == min(splits, max(1, longest // 64))

@@ -92,7 +92,7 @@ def test_ragged_cases(case):
     _full_check(attn, q, k, v, cu, kvs, pre, what="case %d %s" % (case, CASES[case]))
     info = attn.info()
     if splits >= 1:
-        assert info.num_splits == splits
+        assert info.num_splits == PA.planned_splits(splits, pre, [s[2] for s in segs])
 
 
 def test_zero_keys_count_visible_keys():
@@ -182,9 +182,13 @@ def test_chunked_equals_unchunked():
     ch = _attn(hq, hkv, dqk, dv, C, S, splits=1)
     for c0 in range(0, S, C):
         oc, lc = PA.run_chunk(ch, q[c0:], k, v, [0, C], [0], [c0])
-        # tile-aligned chunk boundaries, no split: the same arithmetic in the same order
-        assert torch.equal(oc, of[c0:c0 + C]), "chunk at %d differs" % c0
-        assert torch.equal(lc, lf[:, c0:c0 + C])
+        # tile-aligned chunk boundaries, no split: the same products, summed in an order
+        # that differs only where a tile runs its keys in the other direction (a slot's
+        # second tile streams them descending, and the partner depends on the chunk), so
+        # the results agree to rounding: a bf16 ulp of out (|out| < 0.5 here) and fp32
+        # rounding of lse
+        assert float((oc.double() - of[c0:c0 + C].double()).abs().max()) <= 2.0 ** -9, "chunk at %d" % c0
+        assert float((lc - lf[:, c0:c0 + C]).abs().max()) <= 1e-5
 
 
 def test_gqa_equals_replicated_mha():
@@ -318,7 +322,8 @@ def test_side_stream_and_growing_workspace():
     k = _rand((T, hkv, d), std, 700)
     v = _rand((T, hkv, d), std, 701)
     q = _rand((1024, hq, d), std, 702)
-    cases = [([0, 200], [0], [100]), ([0, 1024], [0], [1900])]   # the second needs more workspace
+    # the second case splits its 2600-key prefix (few workgroups): more workspace
+    cases = [([0, 200], [0], [100]), ([0, 300], [0], [2600])]
     ref = []
     a_ref = ChunkAttention(hq, hkv, d, d, max_chunk_tokens=1024, max_kv_len=T, device="cuda")
     assert a_ref.device == torch.device("cuda", torch.cuda.current_device())
