@@ -124,6 +124,39 @@ vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t plan,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Bytes of device scratch behind vpp_chunk_attn_run_noalloc: one static array
+ * per GPU the library runs on, held until the process ends.
+ */
+#define VPP_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * vpp_chunk_attn_run without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same plan, kernels, arguments and results
+ * as vpp_chunk_attn_run: the same bits, split key ranges included. Its
+ * workspace (the work list and, in split plans, the fp32 partials) is a static
+ * device array of VPP_NOALLOC_SCRATCH_BYTES on the current device, whose
+ * address the library looks up on its first call on that device. This call
+ * makes no hipMalloc, hipFree, host-pinning or other allocating call: the work
+ * list is copied to the device straight from the plan (the copy out of host
+ * memory is complete when the call returns, so the plan may be refilled at
+ * once). Nothing in the scratch needs clearing between calls: every byte a run
+ * reads, the same run writes first.
+ * Calls on one GPU share its array: calls whose work overlaps on that GPU
+ * (several streams, several threads) race and give wrong results; serialize
+ * them. Errors: VPP_ERR_WORKSPACE when the plan needs more than
+ * VPP_NOALLOC_SCRATCH_BYTES (vpp_chunk_attn_plan's workspace size; large split
+ * plans do), VPP_ERR_HIP when the array cannot be found on the current device,
+ * and every error of vpp_chunk_attn_run.
+ */
+vpp_status_t vpp_chunk_attn_run_noalloc(vpp_chunk_attn_plan_t plan,
+                                        const void* q, int64_t q_stride_tok, int64_t q_stride_head,
+                                        const void* k_cache, int64_t k_stride_tok, int64_t k_stride_head,
+                                        const void* v_cache, int64_t v_stride_tok, int64_t v_stride_head,
+                                        void* out, int64_t o_stride_tok, int64_t o_stride_head,
+                                        float* lse, int64_t lse_stride_head, void* stream);
+
+/*
  * Split key layout of the MLA models the paper evaluates (section 6.1: its
  * DeepSeek model runs MLA attention, MHA-style in prefill): each key is the
  * concatenation of a per-head part and a part shared by all heads,

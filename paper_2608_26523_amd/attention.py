@@ -2,9 +2,11 @@
 
 ``ChunkAttention`` validates tensors, owns a plan and a device workspace, and
 passes raw pointers and element strides to ``vpp_chunk_attn_plan`` /
-``vpp_chunk_attn_run`` (contiguous cache), ``vpp_chunk_attn_run_paged`` (paged
-cache) or ``vpp_chunk_attn_run_mla`` (keys split into per-head and shared parts); ``kv_append_paged`` wraps ``vpp_kv_append_paged``. Nothing here does
-arithmetic of its own.
+``vpp_chunk_attn_run`` (contiguous cache), ``vpp_chunk_attn_run_noalloc`` (the
+same without a workspace), ``vpp_chunk_attn_run_paged`` (paged cache) or
+``vpp_chunk_attn_run_mla`` (keys split into per-head and shared parts);
+``kv_append_paged`` wraps ``vpp_kv_append_paged``. Nothing here does arithmetic
+of its own.
 """
 from __future__ import annotations
 
@@ -123,17 +125,8 @@ class ChunkAttention:
             lse_ptr, lse_sh = lse.data_ptr(), lse.stride(0)
         return out, lse_ptr, lse_sh, new_out
 
-    def run(self, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
-            out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-            stream: Optional[torch.cuda.Stream] = None):
-        """Enqueue the planned chunk on ``stream`` (default: torch's current stream).
-
-        q [tokens, Hq, dqk], k_cache [rows, Hkv, dqk], v_cache [rows, Hkv, dv] bf16;
-        out [tokens, Hq, dv] bf16 (allocated when None); lse an fp32 view whose
-        element [h, r] is chunk row r of head h (e.g. a column slice of a
-        [Hq, seq] tensor), or None.
-        """
-        out, lse_ptr, lse_sh, new_out = self._io(q, out, lse)
+    def _check_cache(self, k_cache: torch.Tensor, v_cache: torch.Tensor):
+        """Checks of a contiguous cache shared by run and run_noalloc."""
         c = self.cfg
         self._check(k_cache, "k_cache", torch.bfloat16, 3)
         self._check(v_cache, "v_cache", torch.bfloat16, 3)
@@ -145,6 +138,19 @@ class ChunkAttention:
             raise ValueError("the planned chunk reads cache rows up to %d but the caches hold "
                              "%d/%d rows" % (self.max_row, k_cache.shape[0], v_cache.shape[0]))
         self._on_device((k_cache, "k_cache"), (v_cache, "v_cache"))
+
+    def run(self, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+            out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+            stream: Optional[torch.cuda.Stream] = None):
+        """Enqueue the planned chunk on ``stream`` (default: torch's current stream).
+
+        q [tokens, Hq, dqk], k_cache [rows, Hkv, dqk], v_cache [rows, Hkv, dv] bf16;
+        out [tokens, Hq, dv] bf16 (allocated when None); lse an fp32 view whose
+        element [h, r] is chunk row r of head h (e.g. a column slice of a
+        [Hq, seq] tensor), or None.
+        """
+        out, lse_ptr, lse_sh, new_out = self._io(q, out, lse)
+        self._check_cache(k_cache, v_cache)
         s = self._stream(stream, new_out)
         B.vpp_chunk_attn_run(self._plan,
                              q.data_ptr(), q.stride(0), q.stride(1),
@@ -153,6 +159,26 @@ class ChunkAttention:
                              out.data_ptr(), out.stride(0), out.stride(1),
                              lse_ptr, lse_sh,
                              self._ws.data_ptr(), self._ws.numel(), s.cuda_stream)
+        return out, lse
+
+    def run_noalloc(self, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                    out: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                    stream: Optional[torch.cuda.Stream] = None):
+        """Like ``run``, through ``vpp_chunk_attn_run_noalloc``: the library's static
+        device scratch replaces this object's workspace, and nothing is allocated
+        (``out`` must be given). Plans needing more than ``NOALLOC_SCRATCH_BYTES``
+        are refused; calls that overlap on one GPU share its scratch and race."""
+        if out is None:
+            raise ValueError("run_noalloc allocates nothing: pass out")
+        out, lse_ptr, lse_sh, _ = self._io(q, out, lse)
+        self._check_cache(k_cache, v_cache)
+        s = stream if stream is not None else torch.cuda.current_stream(self.device)
+        B.vpp_chunk_attn_run_noalloc(self._plan,
+                                     q.data_ptr(), q.stride(0), q.stride(1),
+                                     k_cache.data_ptr(), k_cache.stride(0), k_cache.stride(1),
+                                     v_cache.data_ptr(), v_cache.stride(0), v_cache.stride(1),
+                                     out.data_ptr(), out.stride(0), out.stride(1),
+                                     lse_ptr, lse_sh, s.cuda_stream)
         return out, lse
 
     def run_mla(self, q: torch.Tensor, k_nope: torch.Tensor, k_rope: torch.Tensor, v_cache: torch.Tensor,

@@ -25,8 +25,11 @@ EXPORTED = [
     "vpp_chunk_attn_plan", "vpp_chunk_attn_run", "vpp_chunk_attn_destroy",
     "vpp_status_str", "vpp_chunk_attn_plan_info", "vpp_chunk_attn_plan_items",
     "vpp_chunk_attn_run_paged", "vpp_kv_append_paged", "vpp_paged_slot_mapping",
-    "vpp_chunk_attn_run_mla",
+    "vpp_chunk_attn_run_mla", "vpp_chunk_attn_run_noalloc",
 ]
+
+# bytes of the static device scratch behind vpp_chunk_attn_run_noalloc
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class VppError(RuntimeError):
@@ -99,6 +102,9 @@ def load(path: Optional[str] = None):
     lib.vpp_chunk_attn_run_paged.restype = ctypes.c_int
     lib.vpp_chunk_attn_run_paged.argtypes = [vp, vp, i64, i64, vp, i64, i64, i64, vp, i64, i64, i64,
                                              i32, i32, vp, i64, vp, i64, i64, vp, i64, vp, sz, vp]
+    lib.vpp_chunk_attn_run_noalloc.restype = ctypes.c_int
+    lib.vpp_chunk_attn_run_noalloc.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, i64, i64,
+                                               vp, i64, i64, vp, i64, vp]
     lib.vpp_chunk_attn_run_mla.restype = ctypes.c_int
     lib.vpp_chunk_attn_run_mla.argtypes = [vp, vp, i64, i64, vp, i64, i64, vp, i64, vp, i64, i64,
                                            vp, i64, i64, vp, i64, vp, sz, vp]
@@ -149,6 +155,15 @@ def vpp_chunk_attn_run(plan: int, q_ptr: int, q_st: int, q_sh: int, k_ptr: int, 
                                    ws_bytes, stream)
     if st != VPP_OK:
         raise VppError(st, "vpp_chunk_attn_run")
+
+
+def vpp_chunk_attn_run_noalloc(plan: int, q_ptr: int, q_st: int, q_sh: int, k_ptr: int, k_st: int,
+                               k_sh: int, v_ptr: int, v_st: int, v_sh: int, out_ptr: int, o_st: int,
+                               o_sh: int, lse_ptr: int, lse_sh: int, stream: int) -> None:
+    st = load().vpp_chunk_attn_run_noalloc(plan, q_ptr, q_st, q_sh, k_ptr, k_st, k_sh, v_ptr, v_st,
+                                           v_sh, out_ptr, o_st, o_sh, lse_ptr, lse_sh, stream)
+    if st != VPP_OK:
+        raise VppError(st, "vpp_chunk_attn_run_noalloc")
 
 
 def vpp_chunk_attn_run_paged(plan: int, q_ptr: int, q_st: int, q_sh: int, k_ptr: int, k_sp: int,

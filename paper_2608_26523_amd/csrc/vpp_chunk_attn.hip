@@ -1506,10 +1506,17 @@ struct RopeK {
     int64_t kr_st;
 };
 
+// How run_impl puts the work list into the workspace: through the plan's pinned
+// staging ring (asynchronous), or straight from the plan's host copy, which
+// allocates nothing (the copy out of host memory completes before the call
+// returns).
+enum class Upload { staged, direct };
+
 vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int64_t q_sh, const void* k,
                       int64_t k_st, int64_t k_sh, const void* v, int64_t v_st, int64_t v_sh, void* out,
                       int64_t o_st, int64_t o_sh, float* lse, int64_t lse_sh, void* workspace,
-                      size_t workspace_bytes, void* stream_ptr, const PagedKV* pg, const RopeK* rope = nullptr) {
+                      size_t workspace_bytes, void* stream_ptr, const PagedKV* pg, const RopeK* rope = nullptr,
+                      Upload upload = Upload::staged) {
     if (!p) return VPP_ERR_INVALID_ARG;
     if (!q || !k || !v || !out) return VPP_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return VPP_ERR_INVALID_ARG;
@@ -1536,35 +1543,42 @@ vpp_status_t run_impl(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st, int6
     if (p->items.empty()) return VPP_OK;  // nothing to do: every segment is empty
 
     hipStream_t stream = (hipStream_t)stream_ptr;
-    const int slot = p->next_slot;
-    p->next_slot = (p->next_slot + 1) % STAGING_SLOTS;
-    if (!p->staging_done[slot]) {
-        if (hipEventCreateWithFlags(&p->staging_done[slot], hipEventDisableTiming) != hipSuccess)
-            return VPP_ERR_HIP;
-    }
-    if (p->staging_pending[slot]) {
-        if (hipEventSynchronize(p->staging_done[slot]) != hipSuccess) return VPP_ERR_HIP;
-        p->staging_pending[slot] = false;
-    }
-    if (p->staging_cap[slot] < p->items_bytes) {
-        if (p->staging[slot]) (void)hipHostFree(p->staging[slot]);
-        p->staging[slot] = nullptr;
-        p->staging_cap[slot] = 0;
-        if (hipHostMalloc((void**)&p->staging[slot], p->items_bytes, hipHostMallocDefault) != hipSuccess)
-            return VPP_ERR_HIP;
-        p->staging_cap[slot] = p->items_bytes;
-    }
-    memcpy(p->staging[slot], p->items.data(), p->items_bytes);
-    if (pg) {
-        // paged: the kernel finds the segment's block-table row from kv_base
-        for (size_t i = 0; i < p->items.size(); ++i)
-            p->staging[slot][i].kv_base = ((int64_t)p->item_seg[i] << 32) | p->items[i].kv_base;
-    }
     char* ws = (char*)workspace;
-    if (hipMemcpyAsync(ws, p->staging[slot], p->items_bytes, hipMemcpyHostToDevice, stream) != hipSuccess)
-        return VPP_ERR_HIP;
-    if (hipEventRecord(p->staging_done[slot], stream) != hipSuccess) return VPP_ERR_HIP;
-    p->staging_pending[slot] = true;
+    if (upload == Upload::direct) {
+        // the paged path rewrites kv_base in its copy of the list; it always stages
+        if (pg) return VPP_ERR_INVALID_ARG;
+        if (hipMemcpyAsync(ws, p->items.data(), p->items_bytes, hipMemcpyHostToDevice, stream) != hipSuccess)
+            return VPP_ERR_HIP;
+    } else {
+        const int slot = p->next_slot;
+        p->next_slot = (p->next_slot + 1) % STAGING_SLOTS;
+        if (!p->staging_done[slot]) {
+            if (hipEventCreateWithFlags(&p->staging_done[slot], hipEventDisableTiming) != hipSuccess)
+                return VPP_ERR_HIP;
+        }
+        if (p->staging_pending[slot]) {
+            if (hipEventSynchronize(p->staging_done[slot]) != hipSuccess) return VPP_ERR_HIP;
+            p->staging_pending[slot] = false;
+        }
+        if (p->staging_cap[slot] < p->items_bytes) {
+            if (p->staging[slot]) (void)hipHostFree(p->staging[slot]);
+            p->staging[slot] = nullptr;
+            p->staging_cap[slot] = 0;
+            if (hipHostMalloc((void**)&p->staging[slot], p->items_bytes, hipHostMallocDefault) != hipSuccess)
+                return VPP_ERR_HIP;
+            p->staging_cap[slot] = p->items_bytes;
+        }
+        memcpy(p->staging[slot], p->items.data(), p->items_bytes);
+        if (pg) {
+            // paged: the kernel finds the segment's block-table row from kv_base
+            for (size_t i = 0; i < p->items.size(); ++i)
+                p->staging[slot][i].kv_base = ((int64_t)p->item_seg[i] << 32) | p->items[i].kv_base;
+        }
+        if (hipMemcpyAsync(ws, p->staging[slot], p->items_bytes, hipMemcpyHostToDevice, stream) != hipSuccess)
+            return VPP_ERR_HIP;
+        if (hipEventRecord(p->staging_done[slot], stream) != hipSuccess) return VPP_ERR_HIP;
+        p->staging_pending[slot] = true;
+    }
 
     const vpp_chunk_attn_config_t& c = p->cfg;
     AttnArgs a;
@@ -1630,6 +1644,51 @@ extern "C" vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t p, const void* 
                                            void* stream_ptr) {
     return run_impl(p, q, q_st, q_sh, k, k_st, k_sh, v, v_st, v_sh, out, o_st, o_sh, lse, lse_sh, workspace,
                     workspace_bytes, stream_ptr, nullptr);
+}
+
+// ---------------------------------------------------------------------------
+// No-allocation entry point. Its workspace is this file-scope device array (one
+// copy per GPU, held until the process ends). In host code the name `scratch`
+// is only a stand-in for the symbol, never a device address: the array's
+// address on each device is looked up once, with that device current, and kept.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) char scratch[VPP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex scratch_mu;
+void* scratch_addr[MAX_DEVICES] = {};
+
+// The current device's copy of `scratch` (looked up on the first call on that device).
+vpp_status_t scratch_on_current_device(void** addr) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return VPP_ERR_HIP;
+    if (dev >= MAX_DEVICES) return VPP_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_addr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return VPP_ERR_HIP;
+        scratch_addr[dev] = ptr;
+    }
+    *addr = scratch_addr[dev];
+    return VPP_OK;
+}
+
+}  // namespace
+
+extern "C" vpp_status_t vpp_chunk_attn_run_noalloc(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st,
+                                                   int64_t q_sh, const void* k, int64_t k_st, int64_t k_sh,
+                                                   const void* v, int64_t v_st, int64_t v_sh, void* out,
+                                                   int64_t o_st, int64_t o_sh, float* lse, int64_t lse_sh,
+                                                   void* stream_ptr) {
+    if (!p) return VPP_ERR_INVALID_ARG;
+    if (p->ws_bytes > (size_t)VPP_NOALLOC_SCRATCH_BYTES) return VPP_ERR_WORKSPACE;
+    void* ws = nullptr;
+    const vpp_status_t st = scratch_on_current_device(&ws);
+    if (st != VPP_OK) return st;
+    return run_impl(p, q, q_st, q_sh, k, k_st, k_sh, v, v_st, v_sh, out, o_st, o_sh, lse, lse_sh, ws,
+                    (size_t)VPP_NOALLOC_SCRATCH_BYTES, stream_ptr, nullptr, nullptr, Upload::direct);
 }
 
 extern "C" vpp_status_t vpp_chunk_attn_run_mla(vpp_chunk_attn_plan_t p, const void* q, int64_t q_st,

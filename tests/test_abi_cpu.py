@@ -284,6 +284,29 @@ def test_split_key_row_stride_boundary():
         B.vpp_chunk_attn_destroy(h)
 
 
+def test_noalloc_limit_and_refusals_before_any_device_work():
+    """run_noalloc refuses a plan whose workspace exceeds its static scratch, and a NULL
+    plan, before any HIP call; the header's size is the binding's."""
+    import re
+    hdr = open(os.path.join(ROOT, "include", "vpp_chunk_attn.h")).read()
+    m = re.search(r"#define VPP_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", hdr)
+    assert m and int(m.group(1)) << int(m.group(2)) == B.NOALLOC_SCRATCH_BYTES
+    lib = B.load()
+    good = 1 << 20
+    # one 256-row tile, 128 heads, 16 splits over a long prefix: 16 x 256 x 128 x 128 x 4 B of partials
+    c = cfg(hq=128, hkv=128, dqk=192, dv=128, splits=16)
+    h, ws = B.vpp_chunk_attn_plan(c, [0, 256], [0], [500000])
+    try:
+        assert ws > B.NOALLOC_SCRATCH_BYTES
+        st = lib.vpp_chunk_attn_run_noalloc(h, good, 128 * 192, 192, good, 128 * 192, 192, good, 128 * 128,
+                                            128, good, 128 * 128, 128, 0, 0, None)
+        assert st == B.VPP_ERR_WORKSPACE
+    finally:
+        B.vpp_chunk_attn_destroy(h)
+    assert lib.vpp_chunk_attn_run_noalloc(None, good, 1024, 128, good, 256, 128, good, 256, 128,
+                                          good, 1024, 128, 0, 0, None) == B.VPP_ERR_INVALID_ARG
+
+
 def test_empty_chunk_plans_to_nothing():
     info = check_plan(cfg(), [0, 0, 0], [0, 5], [3, 0])
     assert info.num_work_items == 0 and info.num_tokens == 0
