@@ -217,3 +217,60 @@ def test_chunked_prefill_through_paged_cache(dims):
         op, _ = attn_p.run_paged(q[c0:c0 + n], k_pages, v_pages, bt_dev)
         torch.cuda.synchronize()
         assert torch.equal(oc, op), "chunk at %d differs" % c0
+
+
+def test_paged_full_size_mla_last_chunk_pool_over_4gib():
+    """mla's last chunk (prefix 122880, 8192 rows, 128 heads, dims 192/128) over a paged
+    cache of 128-row pages in random order: a 10.7 GB page pool, so page addresses run
+    far past 4 GiB. Sampled (row, head) items against the oracle, evaluated on rows
+    gathered from the pool by the reference page mapping (oracle/paged.contiguous_rows)."""
+    from paper_2608_26523_amd import workloads as W
+    from paper_2608_26523_amd.attention import ChunkAttention
+    w = W.get("mla")
+    c = W.num_chunks(w) - 1
+    t0, cu, kvs, pre = W.chunk_segments(w, c)
+    tok = int(cu[-1])
+    rows = int(pre[0]) + tok
+    page, extra = 128, 4
+    npg = (rows + page - 1) // page
+    print("case: paged mla chunk %d, %d rows in %d pages of %d" % (c, rows, npg, page), flush=True)
+    rng = np.random.default_rng(15)
+    perm = rng.permutation(npg + extra).astype(np.int32)
+    bt = perm[:npg][None, :].copy()
+    std = 1.0 / math.sqrt(w.dqk)
+    idx = torch.as_tensor(bt[0].astype(np.int64), device=DEV)
+    k_pages = torch.full((npg + extra, page, w.hkv, w.dqk), 3.0, dtype=torch.bfloat16, device=DEV)
+    k = W.normal_bf16((rows, w.hkv, w.dqk), std, w.seed, w.index, "k", DEV)
+    k_pages.index_copy_(0, idx, k.view(npg, page, w.hkv, w.dqk))
+    del k
+    v_pages = torch.full((npg + extra, page, w.hkv, w.dv), 3.0, dtype=torch.bfloat16, device=DEV)
+    v = W.normal_bf16((rows, w.hkv, w.dv), std, w.seed, w.index, "v", DEV)
+    v_pages.index_copy_(0, idx, v.view(npg, page, w.hkv, w.dv))
+    del v
+    assert k_pages.numel() * 2 > (4 << 30) and v_pages.numel() * 2 > (4 << 30)
+    q = W.make_q_rows(w, DEV, t0, t0 + tok)
+    attn = ChunkAttention(w.hq, w.hkv, w.dqk, w.dv, max_chunk_tokens=w.chunk, max_kv_len=rows,
+                          num_splits=w.num_splits)
+    attn.plan(cu, [0], pre)
+    out = torch.full((tok, w.hq, w.dv), float("nan"), dtype=torch.bfloat16, device=DEV)
+    lse = torch.full((w.hq, tok), float("nan"), dtype=torch.float32, device=DEV)
+    attn.run_paged(q, k_pages, v_pages, torch.as_tensor(bt, device=DEV), out, lse)
+    torch.cuda.synchronize()
+    r_items, h_items = PA.sample_items(cu, [0], pre, w.hq, w.hkv, seed=c)
+    g = w.hq // w.hkv
+    ro = np.zeros((len(r_items), w.dv))
+    rl = np.zeros(len(r_items))
+    for kvh in sorted(set((h_items // g).tolist())):
+        sel = np.nonzero(h_items // g == kvh)[0]
+        kp = k_pages[:, :, kvh].cpu().view(torch.int16).numpy().view(np.uint16)
+        vp = v_pages[:, :, kvh].cpu().view(torch.int16).numpy().view(np.uint16)
+        kg = OP.contiguous_rows(kp, bt[0], rows)[:, None, :]
+        vg = OP.contiguous_rows(vp, bt[0], rows)[:, None, :]
+        qh = q[:, kvh * g:(kvh + 1) * g].cpu()
+        o, l = oracle.attention(qh, kg, vg, cu, [0], pre, rows=r_items[sel],
+                                heads=h_items[sel] - kvh * g, scale=w.scale)
+        ro[sel], rl[sel] = o, l
+    rep = PA.compare(out, lse, r_items, h_items, ro, rl)
+    print("paged mla chunk %d:" % c, rep, flush=True)
+    assert rep.ok(), rep
+    assert bool(torch.isfinite(out.float()).all())

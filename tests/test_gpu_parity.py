@@ -153,6 +153,52 @@ def test_planted_keys_no_leak():
     assert float(err) <= 1e-2, float(err)
 
 
+@pytest.mark.parametrize("nb", [1, 2])
+@pytest.mark.parametrize("splits", [2, 3, 4])
+def test_planted_keys_across_split_pieces(splits, nb, monkeypatch):
+    """Forced splits: q_i parallel to a key j* that lies in a split piece other than the
+    last, at piece boundaries and key-tile edges (64m - 1, 64m), at key 0, at random
+    earlier keys and on the diagonal. out_i must be v_{j*}; the result must also match
+    the oracle on every item. Several query tiles, so some slots run a tile's keys in
+    descending order."""
+    monkeypatch.setenv("VPP_NB", str(nb))
+    d, dv = 128, 128
+    p, L = 3000, 700
+    T = p + L
+    rng = np.random.default_rng(40 + splits)
+    codes = rng.integers(0, 2, size=(T, d)) * 2 - 1
+    kk = torch.tensor(codes / 8.0, dtype=torch.float32)             # |k|^2 = 2
+    k = kk.to(torch.bfloat16).unsqueeze(1).to(DEV)
+    v = _rand((T, 1, dv), 1.0, 41 + splits)
+    # piece boundaries of an n-way split of the 3000-key prefix (tile-aligned)
+    bounds = [((p // 64) * b // splits) * 64 for b in range(1, splits)]
+    special = [0, 63, 64, 127, 128] + [x for b in bounds for x in (b - 1, b, b + 63, b + 64)]
+    targets = []
+    for r in range(L):
+        i = p + r
+        if r % 4 == 0:
+            j = i                                         # the diagonal
+        elif r % 4 == 1:
+            j = special[(r // 4) % len(special)]          # edges of pieces and tiles
+        elif r % 4 == 2:
+            j = int(rng.integers(0, bounds[-1]))          # somewhere before the last piece
+        else:
+            j = int(rng.integers(0, i + 1))
+        targets.append(j)
+    targets = np.array(targets)
+    assert all(b in targets or b - 1 in targets for b in bounds)
+    q = (kk[targets] * 40.0).to(torch.bfloat16).unsqueeze(1).to(DEV)  # score 80 vs <= ~50
+    attn = _attn(1, 1, d, dv, L, T, splits=splits, scale=1.0)
+    out, lse = PA.run_chunk(attn, q, k, v, [0, L], [0], [p])
+    info = attn.info()
+    assert info.num_splits == splits and info.block_m == 128 * nb
+    want = v[torch.as_tensor(targets, device=DEV), 0]
+    err = (out[:, 0].double() - want.double()).abs().max()
+    assert float(err) <= 1e-2, float(err)
+    _full_check(attn, q, k, v, np.array([0, L]), [0], [p], scale=1.0,
+                what="planted keys, %d splits, nb %d" % (splits, nb))
+
+
 def test_split_matches_unsplit_and_determinism():
     hq, hkv, dqk, dv, p, L = 8, 2, 128, 128, 4000, 384
     T = p + L
