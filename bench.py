@@ -352,6 +352,9 @@ def main():
     ap.add_argument("--no-gemm-ref", action="store_true",
                     help="skip the library GEMM reference taken after the timed steps")
     ap.add_argument("--chunks", type=int, default=0, help="run only the first N chunks")
+    ap.add_argument("--splits", type=int, default=0,
+                    help="split count of the key range (-1 automatic, 1 none, 2..16 fixed); "
+                         "default: the workload's")
     ap.add_argument("--paged", type=int, default=0,
                     help="page size: run the path over a paged KV cache (pages in random order); "
                          "each chunk first appends its own K/V rows into its pages, then attends")
@@ -391,6 +394,9 @@ def main():
     from paper_2608_26523_amd.attention import ChunkAttention
 
     w = W.get(args.workload)
+    if args.splits:
+        import dataclasses
+        w = dataclasses.replace(w, num_splits=args.splits)
     if args.schedule_sweep:
         if w.n_requests != 1:
             print("--schedule-sweep needs a single-request workload", file=sys.stderr)
@@ -416,8 +422,11 @@ def main():
     if args.chunks:
         nchunks = min(nchunks, args.chunks)
     segs = [W.chunk_segments(w, c) for c in range(nchunks)]
-    attn = [ChunkAttention(w.hq, w.hkv, w.dqk, w.dv, max_chunk_tokens=w.chunk,
-                           max_kv_len=S, num_splits=w.num_splits) for _ in range(nchunks)]
+    # one plan and one workspace for the whole prompt: every chunk is planned again right
+    # before its launch, as a serving loop does (the workspace grows to the largest chunk's)
+    attn = ChunkAttention(w.hq, w.hkv, w.dqk, w.dv, max_chunk_tokens=w.chunk, max_kv_len=S,
+                          num_splits=w.num_splits)
+    splits = [0] * nchunks
     flops = [chunk_flops(w, cu, pre)[0] for (_, cu, _, pre) in segs]
     nbytes = [chunk_bytes(w, cu, pre) for (_, cu, _, pre) in segs]
     stream = torch.cuda.current_stream(dev)
@@ -435,7 +444,7 @@ def main():
 
     def step(events=None):
         for c, (t0, cu, kvs, pre) in enumerate(segs):
-            a = attn[c]
+            a = attn
             tok = int(cu[-1])
             if split_keys is not None:
                 a.plan(cu, kvs, pre)
@@ -500,7 +509,8 @@ def main():
     value = total_flops * steps / elapsed / 1e12
     kernel_ms = statistics.fmean(mean)                    # average launch duration
     achieved = (total_flops / nchunks) / (kernel_ms * 1e-3) / 1e12
-    splits = [attn[c].info().num_splits for c in range(nchunks)]
+    for c, (_, cu, kvs, pre) in enumerate(segs):
+        splits[c] = attn.plan(cu, kvs if paged is None else [0] * len(kvs), pre).num_splits
 
     prefix = [int(pre[0]) if len(pre) == 1 else None for (_, _, _, pre) in segs]
     fit = fit_line(list(range(nchunks)), med) if w.n_requests == 1 else None
