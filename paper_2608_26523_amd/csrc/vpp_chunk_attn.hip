@@ -27,6 +27,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <functional>
 #include <type_traits>
 #include <mutex>
 #include <new>
@@ -1264,23 +1265,93 @@ vpp_status_t check_config(const vpp_chunk_attn_config_t& c) {
 // parts common to all of its tiles; the last part runs on to each tile's own end
 // (its keys within the chunk), so pieces of one index read the same keys in every
 // tile. Explicit: the requested count, at most one piece per key tile of the
-// longest prefix (a chunk without a prefix is not split). Automatic: only when
-// the chunk gives too few workgroups to fill the chip, in pieces of at least
-// MIN_PIECE prefix keys.
+// longest prefix (a chunk without a prefix is not split). Automatic: the count
+// whose launch a model of the hardware's workgroup placement finishes first,
+// charging the fp32 partials that a split writes and the merge reads back
+// (see auto_split below); pieces hold at least MIN_PIECE prefix keys, and a
+// split must be predicted to gain at least 3 %.
 constexpr int64_t MIN_PIECE = 1024;
-int choose_splits(const vpp_chunk_attn_config_t& c, int64_t slots, int64_t max_prefix) {
-    if (c.num_splits >= 1)
-        return (int)std::min<int64_t>(c.num_splits, std::max<int64_t>(1, max_prefix / BN));
-    // a slot's two tiles balance each other, so one slot workgroup per CU fills the chip
-    const double wgs = (double)slots * c.num_q_heads;
-    const double target = 256.0;
-    if (wgs >= target) return 1;
-    const int64_t n = (int64_t)ceil(target / std::max(1.0, wgs));
-    return (int)std::max<int64_t>(1, std::min<int64_t>({n, max_prefix / MIN_PIECE, (int64_t)MAX_SPLITS}));
+int fixed_splits(const vpp_chunk_attn_config_t& c, int64_t max_prefix) {
+    return (int)std::min<int64_t>(c.num_splits, std::max<int64_t>(1, max_prefix / BN));
 }
 
 // Boundary b of the n-part split of a p-key prefix (tile-aligned, b = 0 .. n-1).
 int32_t piece_begin(int64_t p, int n, int b) { return (int32_t)(((p / BN) * b / n) * BN); }
+
+// Automatic split count: simulate the launch of each candidate count and keep
+// the fastest. The grid is slots x heads, head-major, remapped so that XCD x
+// runs the x-th eighth of that order (work_coords); each XCD places its
+// workgroups in order on whichever of its CU slots frees first (32 CUs, times
+// the workgroups a CU holds). A workgroup costs its key tiles plus a fixed
+// amount per tile it runs (Q load, pipeline fill, store). A split count n > 1
+// also costs the fp32 partials its pieces write and the merge reads back. The
+// unsplit plan is kept whenever its simulated makespan is within 5 % of the
+// ideal (total work spread evenly), which covers every chunk with enough even
+// slots.
+template <typename Build>
+int auto_split(const vpp_chunk_attn_config_t& c, int bm, int wg_per_cu, int64_t max_prefix, int32_t tokens,
+               Build&& build) {
+    constexpr int NXCD = 8, CU_PER_XCD = 32;
+    constexpr double TILE_OVERHEAD = 2.0;  // fixed cost of a tile, in key tiles
+    const int heads = c.num_q_heads;
+    // one key tile of one workgroup: 2 bm BN (dqk + dv) flop at ~5 TFLOP/s per CU
+    const double tile_s = 2.0 * bm * BN * (c.head_dim_qk + c.head_dim_v) / 5.0e12;
+    std::vector<WorkItem> list;
+    auto entry_cost = [](const WorkItem& w) {
+        return w.nrows ? (double)((w.key_end - w.key_begin + BN - 1) / BN) + TILE_OVERHEAD : 0.0;
+    };
+    // simulated seconds of the launch, and of its work spread evenly over the chip
+    auto simulate = [&](int n, double& ideal) {
+        build(n, list);
+        const int64_t nslots = (int64_t)list.size() / 2;
+        std::vector<double> cost((size_t)nslots);
+        double total = 0.0;
+        for (int64_t i = 0; i < nslots; ++i) {
+            cost[(size_t)i] = entry_cost(list[(size_t)(2 * i)]) + entry_cost(list[(size_t)(2 * i + 1)]);
+            total += cost[(size_t)i];
+        }
+        const int lanes = CU_PER_XCD * wg_per_cu;
+        ideal = total * heads / (NXCD * lanes) * tile_s;
+        const int64_t all = nslots * heads, per = all / NXCD;
+        double makespan = 0.0;
+        std::vector<double> free_at;
+        // with whole heads per XCD every XCD runs the same sequence: one suffices
+        const int xcds = heads % NXCD == 0 ? 1 : NXCD;
+        for (int x = 0; x < xcds; ++x) {
+            free_at.assign((size_t)lanes, 0.0);  // a min-heap of lane free times
+            auto place = [&](int64_t logical) {
+                std::pop_heap(free_at.begin(), free_at.end(), std::greater<double>());
+                free_at.back() += cost[(size_t)(logical % nslots)];
+                std::push_heap(free_at.begin(), free_at.end(), std::greater<double>());
+            };
+            for (int64_t j = 0; j < per; ++j) place(x * per + j);
+            for (int64_t L = per * NXCD + x; L < all; L += NXCD) place(L);  // the part left unremapped
+            makespan = std::max(makespan, *std::max_element(free_at.begin(), free_at.end()));
+        }
+        return makespan * tile_s;
+    };
+    double ideal1 = 0.0;
+    const double t1 = simulate(1, ideal1);
+    if (t1 <= 1.05 * ideal1) return 1;
+    const int64_t cap = std::min<int64_t>(MAX_SPLITS, max_prefix / MIN_PIECE);
+    // partial bytes per piece: fp32 out and lse of every (row, head), written once and
+    // read once, at the ~3 TB/s the split chunks of the mixed workload were measured to
+    // pay; a split must also be predicted to gain at least 3 %
+    const double partial_s = 2.0 * tokens * heads * (4.0 * c.head_dim_v + 4.0) / 3.0e12;
+    int best = 1;
+    double best_t = 0.97 * t1;
+    static const int candidates[] = {2, 3, 4, 6, 8, 12, 16};
+    for (int n : candidates) {
+        if (n > cap) break;
+        double ideal = 0.0;
+        const double t = simulate(n, ideal) + n * partial_s;
+        if (t < best_t) {
+            best_t = t;
+            best = n;
+        }
+    }
+    return best;
+}
 
 }  // namespace
 
@@ -1338,7 +1409,7 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
         struct Seg { int t0, t1; };  // the segment's tiles in `tiles`
         std::vector<WorkItem> tiles;
         std::vector<Seg> segs((size_t)num_segments);
-        int64_t slots = 0, max_prefix = 0;
+        int64_t max_prefix = 0;
         for (int s = 0; s < num_segments; ++s) {
             segs[s].t0 = (int)tiles.size();
             for (int r0 = cu_q[s]; r0 < cu_q[s + 1]; r0 += BM) {
@@ -1355,50 +1426,67 @@ extern "C" vpp_status_t vpp_chunk_attn_plan(const vpp_chunk_attn_config_t* cfg, 
                 pairs += (double)w.nrows * (double)w.pos0 + 0.5 * (double)w.nrows * (w.nrows + 1);
             }
             segs[s].t1 = (int)tiles.size();
-            slots += (segs[s].t1 - segs[s].t0 + 1) / 2;
             if (segs[s].t1 > segs[s].t0) max_prefix = std::max(max_prefix, prefix_len[s]);
         }
         ntiles = (int)tiles.size();
-        nsplit = ntiles ? choose_splits(c, slots, max_prefix) : 1;
 
-        struct Group { int seg, piece; int64_t len; size_t first, count; };  // slots [first, first+count)
-        std::vector<Group> groups;
-        std::vector<WorkItem> grouped;  // two items per slot, group by group
-        const WorkItem none = {0, 0, 0, 0, 0, 0, 0};
-        for (int s = 0; s < num_segments; ++s) {
-            const int T = segs[s].t1 - segs[s].t0;
-            if (T == 0) continue;
-            for (int b = 0; b < nsplit; ++b) {
-                auto piece = [&](int ti) {
-                    WorkItem w = tiles[segs[s].t0 + ti];
-                    w.split = b;
-                    if (nsplit > 1) {
-                        w.key_begin = piece_begin(prefix_len[s], nsplit, b);
-                        if (b + 1 < nsplit) w.key_end = piece_begin(prefix_len[s], nsplit, b + 1);
+        // the work list for n split pieces: two entries per slot, grouped by
+        // (segment, piece), longest group first
+        auto build = [&](int n, std::vector<WorkItem>& out, std::vector<int32_t>* out_seg) {
+            struct Group { int seg, piece; int64_t len; size_t first, count; };  // slots [first, first+count)
+            std::vector<Group> groups;
+            std::vector<WorkItem> grouped;  // two items per slot, group by group
+            const WorkItem none = {0, 0, 0, 0, 0, 0, 0};
+            for (int s = 0; s < num_segments; ++s) {
+                const int T = segs[s].t1 - segs[s].t0;
+                if (T == 0) continue;
+                for (int b = 0; b < n; ++b) {
+                    auto piece = [&](int ti) {
+                        WorkItem w = tiles[segs[s].t0 + ti];
+                        w.split = b;
+                        if (n > 1) {
+                            w.key_begin = piece_begin(prefix_len[s], n, b);
+                            if (b + 1 < n) w.key_end = piece_begin(prefix_len[s], n, b + 1);
+                        }
+                        return w;
+                    };
+                    Group g{s, b, 0, grouped.size() / 2, 0};
+                    for (int i = 0; i < (T + 1) / 2; ++i) {
+                        const WorkItem x = piece(i);
+                        const WorkItem y = (T - 1 - i != i) ? piece(T - 1 - i) : none;
+                        grouped.push_back(x);
+                        grouped.push_back(y);
+                        const int64_t len =
+                            (int64_t)(x.key_end - x.key_begin) + (y.nrows ? y.key_end - y.key_begin : 0);
+                        g.len = std::max(g.len, len);
+                        ++g.count;
                     }
-                    return w;
-                };
-                Group g{s, b, 0, grouped.size() / 2, 0};
-                for (int i = 0; i < (T + 1) / 2; ++i) {
-                    const WorkItem x = piece(i);
-                    const WorkItem y = (T - 1 - i != i) ? piece(T - 1 - i) : none;
-                    grouped.push_back(x);
-                    grouped.push_back(y);
-                    const int64_t len = (int64_t)(x.key_end - x.key_begin) + (y.nrows ? y.key_end - y.key_begin : 0);
-                    g.len = std::max(g.len, len);
-                    ++g.count;
+                    groups.push_back(g);
                 }
-                groups.push_back(g);
             }
+            std::stable_sort(groups.begin(), groups.end(),
+                             [](const Group& x, const Group& y) { return x.len > y.len; });
+            out.clear();
+            out.reserve(grouped.size());
+            if (out_seg) {
+                out_seg->clear();
+                out_seg->reserve(grouped.size());
+            }
+            for (const Group& g : groups)
+                for (size_t k = 0; k < 2 * g.count; ++k) {
+                    out.push_back(grouped[2 * g.first + k]);
+                    if (out_seg) out_seg->push_back(g.seg);
+                }
+        };
+        if (ntiles == 0) {
+            nsplit = 1;
+        } else if (c.num_splits >= 1) {
+            nsplit = fixed_splits(c, max_prefix);
+        } else {
+            nsplit = auto_split(c, BM, nb == 1 ? 2 : 1, max_prefix, cu_q[num_segments],
+                                [&](int n, std::vector<WorkItem>& out) { build(n, out, nullptr); });
         }
-        std::stable_sort(groups.begin(), groups.end(), [](const Group& x, const Group& y) { return x.len > y.len; });
-        items.reserve(grouped.size());
-        iseg.reserve(grouped.size());
-        for (const Group& g : groups)
-            for (size_t k = 0; k < 2 * g.count; ++k) {
-                items.push_back(grouped[2 * g.first + k]);
-                iseg.push_back(g.seg);
-            }
+        build(nsplit, items, &iseg);
     } catch (const std::bad_alloc&) {
         return VPP_ERR_NOMEM;
     }

@@ -213,6 +213,25 @@ def test_auto_split_only_when_few_workgroups():
     assert info.num_splits == 1
 
 
+def test_auto_split_follows_the_simulated_launch():
+    """Automatic splits come from a model of the launch: a chunk whose work sits in a few
+    long slots of one segment (mixed chunk 98: 43 rows behind a 118844-key prefix, next to
+    two short requests) is split; chunks whose slots fill the chip evenly are not."""
+    w = W.get("mixed")
+    c = cfg(hq=w.hq, hkv=w.hkv, dqk=w.dqk, dv=w.dv, max_tok=w.chunk, max_kv=W.total_tokens(w), max_seg=256)
+    _, cu, ks, pl = W.chunk_segments(w, 98)
+    assert len(ks) == 3 and int(max(pl)) > 100000
+    assert check_plan(c, cu, ks, pl).num_splits > 1
+    _, cu, ks, pl = W.chunk_segments(w, 200)        # one request deep in its prefix, one fresh
+    assert check_plan(c, cu, ks, pl).num_splits > 1
+    for name in ("gqa", "mla"):
+        w = W.get(name)
+        c = cfg(hq=w.hq, hkv=w.hkv, dqk=w.dqk, dv=w.dv, max_tok=w.chunk, max_kv=w.seq_len)
+        for k in range(W.num_chunks(w)):
+            _, cu, ks, pl = W.chunk_segments(w, k)
+            assert check_plan(c, cu, ks, pl).num_splits == 1, (name, k)
+
+
 def test_run_argument_checks_before_any_device_work():
     """Errors the host can detect are returned before any HIP call (works without a GPU)."""
     lib = B.load()
