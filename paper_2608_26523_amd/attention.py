@@ -173,12 +173,16 @@ class ChunkAttention:
         out, lse_ptr, lse_sh, _ = self._io(q, out, lse)
         self._check_cache(k_cache, v_cache)
         s = stream if stream is not None else torch.cuda.current_stream(self.device)
-        B.vpp_chunk_attn_run_noalloc(self._plan,
-                                     q.data_ptr(), q.stride(0), q.stride(1),
-                                     k_cache.data_ptr(), k_cache.stride(0), k_cache.stride(1),
-                                     v_cache.data_ptr(), v_cache.stride(0), v_cache.stride(1),
-                                     out.data_ptr(), out.stride(0), out.stride(1),
-                                     lse_ptr, lse_sh, s.cuda_stream)
+        if s.device != self.device:
+            raise ValueError("stream is on %s but the tensors are on %s" % (s.device, self.device))
+        # the library takes the scratch of the current device: make it the tensors' device
+        with torch.cuda.device(self.device):
+            B.vpp_chunk_attn_run_noalloc(self._plan,
+                                         q.data_ptr(), q.stride(0), q.stride(1),
+                                         k_cache.data_ptr(), k_cache.stride(0), k_cache.stride(1),
+                                         v_cache.data_ptr(), v_cache.stride(0), v_cache.stride(1),
+                                         out.data_ptr(), out.stride(0), out.stride(1),
+                                         lse_ptr, lse_sh, s.cuda_stream)
         return out, lse
 
     def run_mla(self, q: torch.Tensor, k_nope: torch.Tensor, k_rope: torch.Tensor, v_cache: torch.Tensor,
