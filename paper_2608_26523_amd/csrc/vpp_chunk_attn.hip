@@ -5,20 +5,24 @@
 // prefix .. prefix+len-1 attending to the cached prefix plus the chunk itself
 // (section 2.4). Several requests may share a chunk (packing, section 5.3).
 //
-// Kernel layout (one workgroup = 4 waves = one tile of 128 query rows of one
-// query head; keys stream through LDS 64 at a time):
+// Kernel layout: one workgroup = 4 waves running one work slot of one query
+// head: up to two query tiles of 256 (or 128) rows of one segment, the first
+// with its keys ascending, the second -- its partner from the other end of the
+// segment -- descending, so that the workgroups on an XCD read the same keys
+// at the same time. Keys stream through LDS 64 at a time:
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16: keys are the M dimension,
 //     queries the N dimension, head dim the K dimension. Each lane then owns
 //     one query (column lane%32) and 16 keys per 32-key block, so a row max or
 //     row sum needs only one exchange with lane^32.
 //   * Online softmax in fp32 with exp2 (scale folded with log2 e).
 //   * O^T = V^T P^T on the same MFMA: P leaves the S^T accumulators already in
-//     the B-operand layout (no shuffles); V is staged transposed in LDS so that
-//     each lane reads its 8 keys of one value column with two 8-byte reads.
+//     the B-operand layout (no shuffles); each lane reads its 8 keys of one
+//     value column from the row-major V tile with two transposing 8-byte LDS
+//     reads (ds_read_b64_tr_b16).
 //   * Only key tiles that cross the diagonal (or the end of the key range) are
-//     masked; tiles past a wave's last query are skipped by that wave.
-//   * Split-KV: a tile's key range may be cut into pieces whose fp32 partial
-//     results are merged by their log-sum-exp in a second pass.
+//     masked; every wave computes every key tile of its workgroup's range.
+//   * Split-KV: the prefix of a segment may be cut into pieces whose fp32
+//     partial results are merged by their log-sum-exp in a second pass.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
