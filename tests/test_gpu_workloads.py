@@ -145,6 +145,10 @@ def test_long_every_chunk_split():
 
 
 def test_mixed_chunks():
+    """Sampled oracle parity on the mixed workload's packed chunks: the first and last, the
+    one packing most requests, the deepest single-request chunk, every chunk of three or
+    more requests, every chunk the automatic split count cuts, and every 32nd chunk."""
+    from paper_2608_26523_amd import binding as B
     from paper_2608_26523_amd import workloads as W
     w = W.get("mixed")
     n = W.num_chunks(w)
@@ -152,11 +156,23 @@ def test_mixed_chunks():
     most = max(range(n), key=lambda c: len(segs[c][2]))
     single = [c for c in range(n) if len(segs[c][2]) == 1]
     deepest = max(single, key=lambda c: int(segs[c][3][0]))
-    # chunk 98: 43 rows behind a 118844-key prefix next to two short requests; the
-    # automatic split count of its simulated launch cuts it four ways
-    picks = sorted({0, most, deepest, 98, n - 1})
     assert int(segs[deepest][3][0]) >= 65536
     assert int(segs[n - 1][1][-1]) < w.chunk or W.total_tokens(w) % w.chunk == 0
+    # the split counts the planner picks (host only)
+    cfg = B.Config(num_q_heads=w.hq, num_kv_heads=w.hkv, head_dim_qk=w.dqk, head_dim_v=w.dv,
+                   softmax_scale=0.0, causal=1, max_chunk_tokens=w.chunk, max_segments=256,
+                   max_kv_len=W.total_tokens(w), num_splits=w.num_splits)
+    planned = {}
+    for c in range(n):
+        h, _ = B.vpp_chunk_attn_plan(cfg, segs[c][1], segs[c][2], segs[c][3])
+        planned[c] = B.vpp_chunk_attn_plan_info(h).num_splits
+        B.vpp_chunk_attn_destroy(h)
+    split = [c for c in range(n) if planned[c] > 1]
+    packed = [c for c in range(n) if len(segs[c][2]) >= 3]
+    # chunk 98: 43 rows behind a 118844-key prefix next to two short requests; the
+    # simulated launch cuts it four ways
+    assert 98 in split and len(split) >= 8 and len(packed) >= 8
+    picks = sorted({0, most, deepest, n - 1} | set(split) | set(packed) | set(range(0, n, 32)))
     k, v = _kv(w, W.total_tokens(w))
     attn = _attn(w, W.total_tokens(w))
     for c in picks:
@@ -164,9 +180,8 @@ def test_mixed_chunks():
         q = W.make_q_rows(w, DEV, t0, t0 + int(cu[-1]))
         info = _check_chunk(w, attn, q, k, v, cu, kvs, pre,
                             "mixed chunk %d (%d segments, first prefix %d)" % (c, len(kvs), int(pre[0])),
-                            seed=c)
-        if c == 98:
-            assert info.num_splits > 1
+                            seed=c, properties=c in {0, most, deepest, 98, n - 1})
+        assert info.num_splits == planned[c]
         del q
     del k, v
     torch.cuda.empty_cache()
