@@ -385,6 +385,13 @@ struct Schedule {
         for (int s = NS - 1; s >= 0; --s)
             if (kind[s] == 1 && s < rescale_before) rescale_before = s;
     }
+    // MFMA slots after the last S^T MFMA of the step
+    constexpr int qk_tail() const {
+        int last = -1;
+        for (int s = 0; s < NS; ++s)
+            if (kind[s] == 0) last = s;
+        return NS - 1 - last;
+    }
     // every O^T MFMA comes after the atoms it depends on; atoms run in order
     constexpr bool valid() const {
         for (int s = 0; s < NS; ++s) {
@@ -403,9 +410,12 @@ struct Schedule {
 // writes it in place) and Q in AGPRs (only MFMAs read it). The compiler cannot
 // see the latency of these instructions, so the schedule keeps the distance
 // itself: an S^T tile is read by VALU code only in the next tile's step (after
-// a barrier). The O^T MFMAs use the builtin, so the compiler tracks their
-// operand hazards (P packed by VALU code just before) and keeps O in AGPRs;
-// the asm that rescales O in place runs only after an explicit drain.
+// a barrier), and every step ends with at least four O^T MFMAs after its last
+// S^T MFMA (checked in the kernel), each occupying the matrix core for longer
+// than an S^T result takes to reach its registers. The O^T MFMAs use the
+// builtin, so the compiler tracks their operand hazards (P packed by VALU code
+// just before) and keeps O in AGPRs; the asm that rescales O in place runs only
+// after an explicit drain.
 #define MFMA_32x32x16_INIT(acc, a, b) \
     asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b))
 #define MFMA_32x32x16_ACC(acc, a, b) \
@@ -520,6 +530,7 @@ void attn_fwd_kernel(AttnArgs a) {
     typedef Schedule<T::NQK, T::NPV, DB, NB> SchedFull;
     typedef Schedule<0, T::NPV, DB, NB> SchedLast;
     static_assert(SchedFull().valid() && SchedLast().valid(), "tile schedule breaks a dependency");
+    static_assert(SchedFull().qk_tail() >= 4, "the next step's softmax could read S^T before it lands");
 
     __shared__ __attribute__((aligned(1024))) char smem[T::BYTES];
     char* const kbuf0 = smem;
