@@ -138,14 +138,16 @@ vpp_status_t vpp_chunk_attn_run(vpp_chunk_attn_plan_t plan,
  * device array of VPP_NOALLOC_SCRATCH_BYTES on the current device, whose
  * address the library looks up on its first call on that device. This call
  * makes no hipMalloc, hipFree, host-pinning or other allocating call: the work
- * list is copied to the device straight from the plan (the copy out of host
- * memory is complete when the call returns, so the plan may be refilled at
- * once). Nothing in the scratch needs clearing between calls: every byte a run
- * reads, the same run writes first.
+ * list is copied to the device straight from the plan, whose host memory is
+ * not pinned; HIP performs such a copy synchronously, so it is complete when
+ * the call returns and the plan may be refilled at once. Nothing in the scratch
+ * needs clearing between calls: every byte a run reads, the same run writes
+ * first.
  * The array used is the current device's (hipGetDevice at the call): the
  * stream and every pointer must belong to that device. Calls on one GPU share
  * its array: calls whose work overlaps on that GPU (several streams, several
- * threads) race and give wrong results; serialize them. Errors: VPP_ERR_WORKSPACE when the plan needs more than
+ * threads) race and give wrong results; serialize them.
+ * Errors: VPP_ERR_WORKSPACE when the plan needs more than
  * VPP_NOALLOC_SCRATCH_BYTES (vpp_chunk_attn_plan's workspace size; large split
  * plans do), VPP_ERR_HIP when the array cannot be found on the current device,
  * and every error of vpp_chunk_attn_run.
